@@ -1,0 +1,214 @@
+/*
+ * acceptmoe.h -- C ABI of the MI355X (gfx950) verify-block MoE layer.
+ *
+ * The layer follows "AcceptMoE: Commitment-Weighted Self-Sizing Verifier
+ * Expert Sets for Efficient MoE Speculative Decoding" (arXiv 2608.02989):
+ * one MoE layer of one speculative-decoding verification block, with the
+ * eligible expert set chosen from commitment-weighted router demand.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers owned by the caller, row-major
+ *    and contiguous, unless an argument says "host".  The library allocates
+ *    no device memory and keeps no state between calls.
+ *  - Every call is asynchronous on `stream` (a hipStream_t passed as void*,
+ *    NULL = the default stream) and never synchronises the host, so a whole
+ *    route -> select -> forward sequence can be captured in a HIP graph.
+ *  - Return value: ACCEPTMOE_OK (0) or a negative ACCEPTMOE_ERR_* code.  All
+ *    argument checks run on the host before any HIP call, so a rejected call
+ *    launches nothing and touches no memory.  acceptmoe_last_error() then
+ *    returns a thread-local, human-readable reason.
+ *  - Contents of device arrays (tree structure, probabilities, routing
+ *    indices) are checked by the kernels themselves: malformed trees are
+ *    reported through `stats`, out-of-range routing indices are skipped.
+ *    Logits or activations that are NaN or Inf give unspecified (but
+ *    memory-safe) results.
+ *  - Calls that share a workspace must be stream-ordered.
+ */
+#ifndef ACCEPTMOE_H
+#define ACCEPTMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define ACCEPTMOE_OK 0
+#define ACCEPTMOE_ERR_INVALID_ARG (-1) /* null pointer, bad size, bad enum      */
+#define ACCEPTMOE_ERR_UNSUPPORTED (-2) /* shape outside the supported limits    */
+#define ACCEPTMOE_ERR_WORKSPACE (-3)   /* workspace pointer/size too small      */
+#define ACCEPTMOE_ERR_HIP (-4)         /* a HIP launch or runtime call failed   */
+
+/* element types */
+#define ACCEPTMOE_F32 0
+#define ACCEPTMOE_BF16 1
+
+/* eligible-set rules (acceptmoe_select `mode`) */
+#define ACCEPTMOE_MODE_SELF_SIZING 0  /* AcceptMoE: anchor + effective rank (Sec. 3.3)   */
+#define ACCEPTMOE_MODE_ALL_EXPERTS 1  /* S = [E]: natural routing, Standard SD (Sec. 3.1) */
+#define ACCEPTMOE_MODE_FIXED_BUDGET 2 /* AcceptMoE-B: anchor + top of R by u, |S| = B (Sec. 4) */
+#define ACCEPTMOE_MODE_MOESPEC 3      /* top-B by summed router mass (Sec. 4 baseline)  */
+#define ACCEPTMOE_MODE_COUNT 4        /* top-B by natural top-k votes (Sec. 4 baseline) */
+
+/* per-tree statistics row written by acceptmoe_select (int32 each) */
+#define ACCEPTMOE_STAT_T 0         /* nodes in the tree                            */
+#define ACCEPTMOE_STAT_ANCHOR 1    /* |A|, root natural top-k (Eq. 5)              */
+#define ACCEPTMOE_STAT_NER 2       /* n_er (Eq. 6) or non-anchor members taken     */
+#define ACCEPTMOE_STAT_S 3         /* |S| before pruning                           */
+#define ACCEPTMOE_STAT_SPRIME 4    /* |S'| after residency pruning (Eq. 7)         */
+#define ACCEPTMOE_STAT_UNAT 5      /* |U_nat|, natural union (Eq. 1)               */
+#define ACCEPTMOE_STAT_BUDGET 6    /* rerouting budget a(S) (Sec. 3.4)             */
+#define ACCEPTMOE_STAT_MSTAR 7     /* m*, experts removed by pruning (Eq. 7)       */
+#define ACCEPTMOE_STAT_CODE 8      /* 0 = ok, else ACCEPTMOE_TREE_* below          */
+#define ACCEPTMOE_STAT_ROUTED 9    /* experts that receive a token of this tree    */
+#define ACCEPTMOE_NUM_STATS 10
+
+/* tree validation codes (the smallest applicable code is reported) */
+#define ACCEPTMOE_TREE_OK 0
+#define ACCEPTMOE_TREE_EMPTY 1       /* tree with no node                              */
+#define ACCEPTMOE_TREE_BAD_ROOT 2    /* first node is not a root (parent -1, depth 0)  */
+#define ACCEPTMOE_TREE_BAD_PARENT 3  /* a later node's parent is not an earlier node
+                                        of the same tree                               */
+#define ACCEPTMOE_TREE_BAD_DEPTH 4   /* depth != parent depth + 1 (or out of range)    */
+#define ACCEPTMOE_TREE_BAD_PROB 5    /* commitment probability < 0 or not finite       */
+
+/* supported limits */
+#define ACCEPTMOE_MAX_EXPERTS 512
+#define ACCEPTMOE_MAX_TOPK 32
+#define ACCEPTMOE_MAX_TREES 256
+#define ACCEPTMOE_MAX_TREE_NODES 1024
+
+/*
+ * acceptmoe_route -- router logits z_t = W_r h_t for every node of the block
+ * (Sec. 3.1, the target-router logits z_t the selector consumes).
+ *
+ *   hidden        [T, H] device, element type `hidden_dtype` (F32 or BF16)
+ *   router_w      [E, H] device fp32 (nn.Linear orientation)
+ *   logits        [T, E] device fp32, written
+ *   T >= 0 (T == 0 is a no-op), 1 <= E <= ACCEPTMOE_MAX_EXPERTS,
+ *   H >= 16 and H % 16 == 0.
+ * Accumulation is fp32; the result is deterministic (fixed reduction order).
+ */
+int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const float* router_w,
+                        int32_t T, int32_t H, int32_t E, float* logits, void* stream);
+
+/*
+ * acceptmoe_select_workspace_size -- bytes of device workspace acceptmoe_select
+ * needs for T nodes and top-k.  No alignment beyond 256 bytes is required.
+ */
+size_t acceptmoe_select_workspace_size(int32_t T, int32_t E, int32_t k);
+
+/*
+ * acceptmoe_select -- eligible expert set per verification tree and the
+ * restricted routing of every node (Sec. 3.1-3.4, Eq. 1-7).
+ *
+ * Per tree b (nodes tree_offsets[b] .. tree_offsets[b+1]-1):
+ *   r_t = softmax(z_t), K_t = TopK_k(z_t) (Sec. 3.1); votes v_e, U_nat (Eq. 1);
+ *   alpha_t = p_t^beta / sqrt(N_{d_t}) (Eq. 3); u_e = sum_t alpha_t r_{t,e} 1[e in K_t]
+ *   (Eq. 4); A = K_root (Eq. 5); n_er = ceil(exp(H(q)) - 1e-9) over R = [E] \ A
+ *   (Eq. 6); S = A u Top_{n_er}(U_R), |S| >= k (Sec. 3.3); with a residency mask
+ *   the longest prefix of the nonresident members ordered by (u asc, index asc)
+ *   allowed by Eq. 7 is removed, giving S'; finally every node is routed by
+ *   TopK_k(z_t + M_{S'}) (Eq. 2) with gates = softmax over its k selected logits.
+ * Ties in logits (fp32) and in utilities (fp64) go to the lower expert index.
+ *
+ *   logits        [T, E] fp32 device (e.g. from acceptmoe_route)
+ *   parent        [T] int32 device, global node ids, -1 for each tree's root;
+ *                 NULL = not available (only depth ranges are checked)
+ *   depth         [T] int32 device, draft position d_t (tree depth, or block
+ *                 offset for a chain)
+ *   commit_prob   [T] fp32 device, p_{d_t} per node (expand a per-depth table
+ *                 p_hat[d] on the caller side)
+ *   tree_offsets  [B+1] int32 HOST array: 0 = o_0 <= o_1 <= ... <= o_B = T;
+ *                 NULL means one tree holding all T nodes (B must be 1).
+ *                 Read during the call only.  Each tree needs
+ *                 o_{b+1} - o_b <= ACCEPTMOE_MAX_TREE_NODES.
+ *   B             trees, 1 <= B <= ACCEPTMOE_MAX_TREES (T == 0 with B == 0 is a no-op)
+ *   k             top-k, 1 <= k <= min(E, ACCEPTMOE_MAX_TOPK)
+ *   beta          commitment sharpness (paper default 0.5), finite, >= 0
+ *   mode          ACCEPTMOE_MODE_*
+ *   budget        |S| for the fixed-budget modes (clamped to [k, E]); ignored otherwise
+ *   removal_cap   pruning removal cap (Sec. 3.4); < 0 means E (nonbinding)
+ *   resident_mask [E] uint8 device, nonzero = expert resident; NULL = no pruning
+ *                 (full residency).  Shared by all trees.
+ *   eligible      [B, E] uint8 device, written: 1 if e in S'_b
+ *   topk_idx      [T, k] int32 device, written: restricted experts of node t in
+ *                 (logit desc, index asc) order; -1 for nodes of an invalid tree
+ *   topk_gate     [T, k] fp32 device, written: renormalised gates (0 for -1 slots)
+ *   stats         [B, ACCEPTMOE_NUM_STATS] int32 device, written; may be NULL
+ *   workspace     device scratch of acceptmoe_select_workspace_size(T, E, k) bytes
+ */
+int32_t acceptmoe_select(const float* logits, const int32_t* parent, const int32_t* depth,
+                         const float* commit_prob, const int32_t* tree_offsets, int32_t B,
+                         int32_t T, int32_t E, int32_t k, double beta, int32_t mode,
+                         int32_t budget, int32_t removal_cap, const uint8_t* resident_mask,
+                         uint8_t* eligible, int32_t* topk_idx, float* topk_gate, int32_t* stats,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * acceptmoe_packed_weights_bytes -- bytes of a packed expert-weight stack.
+ * acceptmoe_pack_expert_weights -- converts a row-major stack [E, N, K]
+ * (nn.Linear [out, in] per expert) into the MFMA fragment layout the expert
+ * FFN streams: for every expert, every 16-row tile and every K chunk of
+ * 64 bytes per row, the 16 x (64 B) block is stored as 64 lanes x 16 B, lane
+ * L holding row (L % 16), bytes 16*(L / 16) .. +15 of that chunk.  Each wave
+ * load of a weight fragment is then one contiguous 1 KiB read.  The packed
+ * stack has exactly the size of the source.  A one-time, load-time step.
+ *
+ *   src  [E, N, K] device, dtype F32 or BF16;  dst packed, device, same size,
+ *   must not overlap src.  Requires N % 16 == 0 and K % (64 / sizeof(elem)) == 0.
+ * Gate and up stacks are [E, I, H] (N = I, K = H); the down stack is [E, H, I].
+ */
+size_t acceptmoe_packed_weights_bytes(int32_t dtype, int32_t E, int32_t N, int32_t K);
+int32_t acceptmoe_pack_expert_weights(const void* src, int32_t dtype, int32_t E, int32_t N,
+                                      int32_t K, void* dst, void* stream);
+
+/*
+ * acceptmoe_moe_forward_workspace_size -- device workspace bytes for
+ * acceptmoe_moe_forward.
+ */
+size_t acceptmoe_moe_forward_workspace_size(int32_t T, int32_t H, int32_t I, int32_t E,
+                                            int32_t k, int32_t dtype);
+
+/*
+ * acceptmoe_moe_forward -- grouped SwiGLU expert FFN over the restricted
+ * routing (Sec. 3.1, Eq. 2: tokens are dispatched only to experts of S'):
+ *   out_t = sum_j g_{t,j} W_d,e (silu(W_g,e x_t) * W_u,e x_t),  e = topk_idx[t, j].
+ * Only experts that receive at least one token are read, each exactly once.
+ *
+ *   hidden        [T, H] device, element type `dtype`
+ *   w_gate, w_up  packed [E, I, H] stacks (acceptmoe_pack_expert_weights), `dtype`
+ *   w_down        packed [E, H, I] stack, `dtype`
+ *   topk_idx      [T, k] int32 device; entries outside [0, E) are skipped, and an
+ *                 expert repeated within a row is used once (at its first slot)
+ *   topk_gate     [T, k] fp32 device
+ *   out           [T, H] fp32 device, written (every element)
+ *   workspace     acceptmoe_moe_forward_workspace_size(...) bytes
+ *   Limits: H % 32 == 0 and I % 32 == 0 (bf16), H % 16 == 0 and I % 16 == 0
+ *   (fp32); 1 <= E <= ACCEPTMOE_MAX_EXPERTS; 1 <= k <= ACCEPTMOE_MAX_TOPK;
+ *   T == 0 is a no-op.
+ * bf16: MFMA bf16 products with fp32 accumulation; the SwiGLU activation is
+ * rounded to bf16 before the down projection.  fp32: fp32 MFMA throughout.
+ * The result is deterministic (the k expert contributions of a token are
+ * summed in slot order).
+ */
+int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_gate,
+                              const void* w_up, const void* w_down, int32_t T, int32_t H,
+                              int32_t I, int32_t E, int32_t k, const int32_t* topk_idx,
+                              const float* topk_gate, float* out, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/* Thread-local description of the last error (empty string if none). */
+const char* acceptmoe_last_error(void);
+
+/* Library ABI version (major * 100 + minor). */
+int32_t acceptmoe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ACCEPTMOE_H */

@@ -41,7 +41,8 @@ design notes of the repository):
   R13 the fixed-budget rows (AcceptMoE-B, MoE-Spec, Count-B) take |S| = B;
       AcceptMoE-B keeps the anchor and fills with the top of R by u;
       MoE-Spec ranks every expert by sum_t r_{t,e}; Count-B ranks by v_e;
-      both baselines break ties toward the lower index and keep no anchor.
+      both baselines break ties toward the lower index, keep no anchor and
+      are never pruned (residency pruning is a stage of AcceptMoE only).
 """
 from __future__ import annotations
 
@@ -356,10 +357,11 @@ def select_tree(z32, parent, depth, prob, k: int, beta: float = 0.5,
         raise ValueError("unknown mode")
 
     # Sec. 3.4: rerouting budget a(S) (reported always) and residency-aware
-    # pruning (only with a mask, never for natural routing)
-    a_S = int(sum(int(v[e]) for e in U_nat if e not in S))
+    # pruning (only with a mask, and only for AcceptMoE's own selectors:
+    # natural routing and the two baselines never prune)
+    a_S = int(sum(int(v[e]) for e in U_nat if e not in S)) if mode != MODE_ALL_EXPERTS else 0
     m_star, pi = 0, []
-    if resident is not None and mode != MODE_ALL_EXPERTS:
+    if resident is not None and mode in (MODE_SELF_SIZING, MODE_FIXED_BUDGET):
         Sp, a_S, m_star, pi = residency_prune(S, u, v, U_nat, resident, k, removal_cap)
     else:
         Sp = set(S)

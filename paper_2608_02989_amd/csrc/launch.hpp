@@ -1,0 +1,74 @@
+// Host-side launch functions of the kernels (internal to the library; the
+// public boundary is include/acceptmoe.h).  Each returns the HIP status of
+// its launches.  Arguments are already validated by the API layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace amoe {
+
+constexpr int kMaxTrees = 256;
+constexpr int kMaxTreeNodes = 1024;
+constexpr int kMaxExperts = 512;
+constexpr int kMaxTopK = 32;
+constexpr int kNumStats = 10;
+
+// ---- router (route.hip) ----
+hipError_t launch_route(const void* hidden, int hidden_is_bf16, const float* router_w, int T, int H,
+                        int E, float* logits, hipStream_t stream);
+
+// ---- selection (select.hip) ----
+struct TreeOffsets {
+  int32_t o[kMaxTrees + 1];
+};
+
+struct SelectParams {
+  const float* logits;
+  const int32_t* parent;
+  const int32_t* depth;
+  const float* prob;
+  const uint8_t* resident;
+  uint8_t* eligible;
+  int32_t* topk_idx;
+  float* topk_gate;
+  int32_t* stats;
+  int32_t* ws_kidx;   // [T, k] natural top-k (slot order)
+  double* ws_contrib; // [T, k] alpha_t * r_{t,e}
+  double* ws_rfull;   // [T, E] full softmax rows (MoE-Spec mass only)
+  double beta;
+  int T, E, k, B, mode, budget, removal_cap;
+};
+
+size_t select_workspace_bytes(int T, int E, int k);
+void select_carve(void* ws, int T, int E, int k, SelectParams& p);
+hipError_t launch_select(const SelectParams& p, const TreeOffsets& offs, hipStream_t stream);
+
+// ---- expert FFN (forward.hip) ----
+hipError_t launch_pack(const void* src, int is_bf16, int E, int N, int K, void* dst, hipStream_t stream);
+
+struct ForwardParams {
+  const void* hidden;
+  const void* w_gate;
+  const void* w_up;
+  const void* w_down;
+  const int32_t* topk_idx;
+  const float* topk_gate;
+  float* out;
+  // workspace
+  int32_t* cnt;       // [E]
+  int32_t* off;       // [E + 1]
+  int32_t* active;    // [E]
+  int32_t* n_active;  // [1]
+  int32_t* ent_slot;  // [T * k] slot ids grouped by expert, token order
+  void* act;          // [T * k, I] bf16 or fp32
+  float* ys;          // [T * k, H] gate-weighted expert outputs
+  int T, H, I, E, k, is_bf16;
+};
+
+size_t forward_workspace_bytes(int T, int H, int I, int E, int k, int is_bf16);
+void forward_carve(void* ws, ForwardParams& p);
+hipError_t launch_forward(const ForwardParams& p, hipStream_t stream);
+
+}  // namespace amoe

@@ -1,0 +1,87 @@
+// Router logits z_t = W_r h_t (Sec. 3.1): an fp32 [T,H] x [E,H]^T product on
+// the fp32 MFMA (v_mfma_f32_16x16x4f32), one 16-token x 16-expert tile per
+// workgroup, the H reduction split over the 4 waves and combined in LDS in a
+// fixed order (deterministic).
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace amoe {
+
+namespace {
+
+constexpr int kRouteWaves = 4;
+
+__device__ __forceinline__ float4 load4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+
+__device__ __forceinline__ float4 load4(const uint16_t* p) {
+  uint2 v = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                     __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+}
+
+// grid (ceil(E/16), ceil(T/16)), block 256.  Lane (r, g): token row t0 + r of
+// the A tile and expert column e0 + r of the B tile; K slice g of each
+// 16-wide chunk is the float4 at offset 4g, component j feeds MFMA j.
+template <typename TIn>
+__global__ __launch_bounds__(256) void route_kernel(const TIn* __restrict__ hidden,
+                                                    const float* __restrict__ w, int T, int H, int E,
+                                                    float* __restrict__ logits) {
+  __shared__ floatx4 part[kRouteWaves][kWave];
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  const int r = lane & 15, g = lane >> 4;
+  const int e0 = blockIdx.x * 16, t0 = blockIdx.y * 16;
+  const int t = t0 + r, e = e0 + r;
+  const bool tv = t < T, ev = e < E;
+  const TIn* hrow = hidden + static_cast<size_t>(tv ? t : 0) * H + 4 * g;
+  const float* wrow = w + static_cast<size_t>(ev ? e : 0) * H + 4 * g;
+
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  const int nchunk = H / 16;
+#pragma unroll 4
+  for (int c = wave; c < nchunk; c += kRouteWaves) {
+    const int k0 = c * 16;
+    float4 a = tv ? load4(hrow + k0) : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 b = ev ? load4(wrow + k0) : make_float4(0.f, 0.f, 0.f, 0.f);
+    acc = mfma_f32_16x16x4(a.x, b.x, acc);
+    acc = mfma_f32_16x16x4(a.y, b.y, acc);
+    acc = mfma_f32_16x16x4(a.z, b.z, acc);
+    acc = mfma_f32_16x16x4(a.w, b.w, acc);
+  }
+  part[wave][lane] = acc;
+  __syncthreads();
+  if (wave == 0) {
+    floatx4 s = part[0][lane];
+#pragma unroll
+    for (int w2 = 1; w2 < kRouteWaves; ++w2) {
+      floatx4 q = part[w2][lane];
+      s[0] += q[0];
+      s[1] += q[1];
+      s[2] += q[2];
+      s[3] += q[3];
+    }
+    if (ev) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tt = t0 + 4 * g + i;
+        if (tt < T) logits[static_cast<size_t>(tt) * E + e] = s[i];
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_route(const void* hidden, int hidden_is_bf16, const float* router_w, int T, int H,
+                        int E, float* logits, hipStream_t stream) {
+  dim3 grid((E + 15) / 16, (T + 15) / 16);
+  if (hidden_is_bf16)
+    route_kernel<uint16_t><<<grid, 256, 0, stream>>>(static_cast<const uint16_t*>(hidden), router_w,
+                                                     T, H, E, logits);
+  else
+    route_kernel<float><<<grid, 256, 0, stream>>>(static_cast<const float*>(hidden), router_w, T, H,
+                                                  E, logits);
+  return hipGetLastError();
+}
+
+}  // namespace amoe

@@ -1,0 +1,200 @@
+"""Thin torch binding over the C ABI: argument marshalling only.
+
+Every step runs in the HIP kernels of libacceptmoe.so; torch provides device
+memory and the current stream.  Functions raise AcceptMoEError on any status
+other than OK and RuntimeError when the library is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import torch
+
+from . import _lib as L
+from ._lib import AcceptMoEError, check, lib  # noqa: F401
+
+
+def _stream_ptr(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return L.BF16
+    if t.dtype == torch.float32:
+        return L.F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, dim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if dim is not None and t.dim() != dim:
+        raise ValueError(f"{name} must have {dim} dims")
+
+
+# ---------------------------------------------------------------------------
+def route(hidden: torch.Tensor, router_w: torch.Tensor, out: torch.Tensor | None = None,
+          stream=None) -> torch.Tensor:
+    """Router logits [T, E] fp32 (acceptmoe_route)."""
+    _need(hidden, "hidden", dim=2)
+    _need(router_w, "router_w", torch.float32, 2)
+    T, H = hidden.shape
+    E = router_w.shape[0]
+    if router_w.shape[1] != H:
+        raise ValueError("router_w must be [E, H]")
+    if out is None:
+        out = torch.empty((T, E), dtype=torch.float32, device=hidden.device)
+    check(lib().acceptmoe_route(_ptr(hidden), _dtype_code(hidden), _ptr(router_w), T, H, E, _ptr(out),
+                                _stream_ptr(stream)))
+    return out
+
+
+def select_workspace(T: int, E: int, k: int, device) -> torch.Tensor:
+    n = lib().acceptmoe_select_workspace_size(T, E, k)
+    return torch.empty(max(int(n), 256), dtype=torch.uint8, device=device)
+
+
+def select(logits: torch.Tensor, parent: torch.Tensor | None, depth: torch.Tensor, prob: torch.Tensor,
+           tree_offsets=None, k: int = 8, beta: float = 0.5, mode: int = L.MODE_SELF_SIZING,
+           budget: int = 0, removal_cap: int = -1, resident: torch.Tensor | None = None,
+           workspace: torch.Tensor | None = None, outputs: dict | None = None, stream=None) -> dict:
+    """Eligible sets, restricted top-k and gates (acceptmoe_select).
+
+    tree_offsets: host sequence of B+1 ints, or None for one tree.
+    Returns dict(eligible [B,E] uint8, idx [T,k] int32, gate [T,k] fp32, stats [B,10] int32).
+    """
+    _need(logits, "logits", torch.float32, 2)
+    _need(depth, "depth", torch.int32, 1)
+    _need(prob, "prob", torch.float32, 1)
+    if parent is not None:
+        _need(parent, "parent", torch.int32, 1)
+    if resident is not None:
+        _need(resident, "resident", torch.uint8, 1)
+    T, E = logits.shape
+    if tree_offsets is None:
+        offs_arr, B = None, 1
+    else:
+        offs_np = np.ascontiguousarray(np.asarray(tree_offsets, dtype=np.int32))
+        B = len(offs_np) - 1
+        offs_arr = (ctypes.c_int32 * len(offs_np))(*offs_np.tolist())
+    dev = logits.device
+    if outputs is None:
+        outputs = {
+            "eligible": torch.empty((max(B, 1), E), dtype=torch.uint8, device=dev),
+            "idx": torch.empty((T, k), dtype=torch.int32, device=dev),
+            "gate": torch.empty((T, k), dtype=torch.float32, device=dev),
+            "stats": torch.empty((max(B, 1), L.NUM_STATS), dtype=torch.int32, device=dev),
+        }
+    if workspace is None:
+        workspace = select_workspace(T, E, k, dev)
+    check(lib().acceptmoe_select(
+        _ptr(logits), _ptr(parent), _ptr(depth), _ptr(prob), offs_arr, B, T, E, k, float(beta), int(mode),
+        int(budget), int(removal_cap), _ptr(resident), _ptr(outputs["eligible"]), _ptr(outputs["idx"]),
+        _ptr(outputs["gate"]), _ptr(outputs["stats"]), _ptr(workspace), workspace.numel(),
+        _stream_ptr(stream)))
+    return outputs
+
+
+def pack_expert_weights(w: torch.Tensor, stream=None) -> torch.Tensor:
+    """[E, N, K] row-major stack -> packed MFMA fragment layout (same shape and size)."""
+    _need(w, "w", dim=3)
+    E, N, K = w.shape
+    out = torch.empty_like(w)
+    check(lib().acceptmoe_pack_expert_weights(_ptr(w), _dtype_code(w), E, N, K, _ptr(out),
+                                              _stream_ptr(stream)))
+    return out
+
+
+def forward_workspace(T: int, H: int, I: int, E: int, k: int, dtype: torch.dtype, device) -> torch.Tensor:
+    code = L.BF16 if dtype == torch.bfloat16 else L.F32
+    n = lib().acceptmoe_moe_forward_workspace_size(T, H, I, E, k, code)
+    return torch.empty(max(int(n), 256), dtype=torch.uint8, device=device)
+
+
+def moe_forward(hidden: torch.Tensor, w_gate_p: torch.Tensor, w_up_p: torch.Tensor, w_down_p: torch.Tensor,
+                topk_idx: torch.Tensor, topk_gate: torch.Tensor, out: torch.Tensor | None = None,
+                workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Grouped SwiGLU expert FFN over packed weights (acceptmoe_moe_forward) -> [T, H] fp32."""
+    _need(hidden, "hidden", dim=2)
+    for n_, w in (("w_gate", w_gate_p), ("w_up", w_up_p), ("w_down", w_down_p)):
+        _need(w, n_, hidden.dtype, 3)
+    _need(topk_idx, "topk_idx", torch.int32, 2)
+    _need(topk_gate, "topk_gate", torch.float32, 2)
+    T, H = hidden.shape
+    E, I, H2 = w_gate_p.shape
+    k = topk_idx.shape[1]
+    if H2 != H or tuple(w_up_p.shape) != (E, I, H) or tuple(w_down_p.shape) != (E, H, I):
+        raise ValueError("weight stacks must be gate/up [E, I, H] and down [E, H, I]")
+    if tuple(topk_idx.shape) != (T, k) or tuple(topk_gate.shape) != (T, k):
+        raise ValueError("topk_idx / topk_gate must be [T, k]")
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.float32, device=hidden.device)
+    if workspace is None:
+        workspace = forward_workspace(T, H, I, E, k, hidden.dtype, hidden.device)
+    check(lib().acceptmoe_moe_forward(
+        _ptr(hidden), _dtype_code(hidden), _ptr(w_gate_p), _ptr(w_up_p), _ptr(w_down_p), T, H, I, E, k,
+        _ptr(topk_idx), _ptr(topk_gate), _ptr(out), _ptr(workspace), workspace.numel(), _stream_ptr(stream)))
+    return out
+
+
+# ---------------------------------------------------------------------------
+class VerifyLayer:
+    """One MoE layer with packed expert weights and preallocated workspaces.
+
+    step() runs route -> select -> forward for one verification block on the
+    current stream, allocating nothing.
+    """
+
+    def __init__(self, router_w: torch.Tensor, w_gate: torch.Tensor, w_up: torch.Tensor,
+                 w_down: torch.Tensor, k: int, max_tokens: int, max_trees: int = 1, beta: float = 0.5,
+                 mode: int = L.MODE_SELF_SIZING, budget: int = 0, removal_cap: int = -1,
+                 packed: bool = False):
+        self.router_w = router_w
+        self.E, self.I, self.H = w_gate.shape
+        self.k, self.beta, self.mode, self.budget, self.removal_cap = k, beta, mode, budget, removal_cap
+        self.dtype = w_gate.dtype
+        if packed:
+            self.wg, self.wu, self.wd = w_gate, w_up, w_down
+        else:
+            self.wg = pack_expert_weights(w_gate)
+            self.wu = pack_expert_weights(w_up)
+            self.wd = pack_expert_weights(w_down)
+        dev = w_gate.device
+        T = max_tokens
+        self.logits = torch.empty((T, self.E), dtype=torch.float32, device=dev)
+        self.sel_ws = select_workspace(T, self.E, k, dev)
+        self.fwd_ws = forward_workspace(T, self.H, self.I, self.E, k, self.dtype, dev)
+        self.sel_out = {
+            "eligible": torch.empty((max_trees, self.E), dtype=torch.uint8, device=dev),
+            "idx": torch.empty((T, k), dtype=torch.int32, device=dev),
+            "gate": torch.empty((T, k), dtype=torch.float32, device=dev),
+            "stats": torch.empty((max_trees, L.NUM_STATS), dtype=torch.int32, device=dev),
+        }
+        self.out = torch.empty((T, self.H), dtype=torch.float32, device=dev)
+
+    def step(self, hidden, parent, depth, prob, tree_offsets=None, resident=None, stream=None):
+        T = hidden.shape[0]
+        B = 1 if tree_offsets is None else len(tree_offsets) - 1
+        logits = self.logits[:T]
+        route(hidden, self.router_w, out=logits, stream=stream)
+        outs = {"eligible": self.sel_out["eligible"][:B], "idx": self.sel_out["idx"][:T],
+                "gate": self.sel_out["gate"][:T], "stats": self.sel_out["stats"][:B]}
+        select(logits, parent, depth, prob, tree_offsets, self.k, self.beta, self.mode, self.budget,
+               self.removal_cap, resident, workspace=self.sel_ws, outputs=outs, stream=stream)
+        out = self.out[:T]
+        moe_forward(hidden, self.wg, self.wu, self.wd, outs["idx"], outs["gate"], out=out,
+                    workspace=self.fwd_ws, stream=stream)
+        return logits, outs, out

@@ -1,0 +1,140 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, sizes workspaces, and rejects bad arguments on the host
+before any HIP call (every case below fails validation, so nothing is
+launched and no pointer is dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_02989_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "acceptmoe.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="HIP library not built")
+
+V = ctypes.c_void_p
+FAKE = V(0x100000)       # aligned non-null address, never dereferenced (validation fails first)
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(acceptmoe_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = header_functions()
+    assert len(names) >= 9
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(L.SIGNATURES)
+
+
+def test_version_and_error_string():
+    assert L.lib().acceptmoe_version() == 100
+    assert isinstance(L.lib().acceptmoe_last_error(), bytes)
+
+
+def test_workspace_sizes():
+    lib = L.lib()
+    assert lib.acceptmoe_select_workspace_size(32, 128, 8) >= 32 * 8 * 12
+    assert lib.acceptmoe_select_workspace_size(-1, 128, 8) == 0
+    a = lib.acceptmoe_moe_forward_workspace_size(32, 2048, 768, 128, 8, L.BF16)
+    assert a >= 32 * 8 * (768 * 2 + 2048 * 4)
+    assert lib.acceptmoe_moe_forward_workspace_size(32, 2048, 768, 128, 8, 9) == 0
+    assert lib.acceptmoe_packed_weights_bytes(L.BF16, 4, 32, 64) == 4 * 32 * 64 * 2
+    assert lib.acceptmoe_packed_weights_bytes(L.F32, 4, 32, 64) == 4 * 32 * 64 * 4
+
+
+def status_and_msg(rc):
+    return rc, L.lib().acceptmoe_last_error().decode()
+
+
+def test_route_rejects():
+    f = L.lib().acceptmoe_route
+    assert status_and_msg(f(FAKE, L.BF16, FAKE, -1, 256, 16, FAKE, None))[0] == L.ERR_INVALID_ARG
+    assert f(FAKE, L.BF16, FAKE, 8, 256, 0, FAKE, None) == L.ERR_UNSUPPORTED
+    assert f(FAKE, L.BF16, FAKE, 8, 256, 513, FAKE, None) == L.ERR_UNSUPPORTED
+    assert f(FAKE, L.BF16, FAKE, 8, 250, 16, FAKE, None) == L.ERR_UNSUPPORTED
+    assert f(FAKE, 7, FAKE, 8, 256, 16, FAKE, None) == L.ERR_INVALID_ARG
+    rc, msg = status_and_msg(f(None, L.F32, FAKE, 8, 256, 16, FAKE, None))
+    assert rc == L.ERR_INVALID_ARG and "null" in msg
+    assert f(V(0x100004), L.F32, FAKE, 8, 256, 16, FAKE, None) == L.ERR_INVALID_ARG   # misaligned
+    # T == 0 is a no-op
+    assert f(None, L.F32, None, 0, 256, 16, None, None) == L.OK
+
+
+def sel(**kw):
+    a = dict(logits=FAKE, parent=FAKE, depth=FAKE, prob=FAKE, offs=None, B=1, T=8, E=16, k=2, beta=0.5,
+             mode=0, budget=0, cap=-1, res=None, elig=FAKE, idx=FAKE, gate=FAKE, stats=FAKE,
+             ws=None, wsb=0)
+    a.update(kw)
+    offs = a["offs"]
+    offs_arr = None if offs is None else (ctypes.c_int32 * len(offs))(*offs)
+    return L.lib().acceptmoe_select(a["logits"], a["parent"], a["depth"], a["prob"], offs_arr, a["B"],
+                                    a["T"], a["E"], a["k"], a["beta"], a["mode"], a["budget"], a["cap"],
+                                    a["res"], a["elig"], a["idx"], a["gate"], a["stats"], a["ws"],
+                                    a["wsb"], None)
+
+
+def test_select_rejects():
+    assert sel(k=17) == L.ERR_UNSUPPORTED
+    assert sel(k=0) == L.ERR_UNSUPPORTED
+    assert sel(E=600, k=2) == L.ERR_UNSUPPORTED
+    assert sel(E=64, k=33) == L.ERR_UNSUPPORTED
+    assert sel(T=-3) == L.ERR_INVALID_ARG
+    assert sel(B=0) == L.ERR_UNSUPPORTED
+    assert sel(B=257, offs=list(range(258)), T=257) == L.ERR_UNSUPPORTED
+    assert sel(beta=float("nan")) == L.ERR_INVALID_ARG
+    assert sel(beta=-1.0) == L.ERR_INVALID_ARG
+    assert sel(mode=5) == L.ERR_INVALID_ARG
+    assert sel(B=2, offs=None) == L.ERR_INVALID_ARG
+    assert sel(B=2, offs=[1, 4, 8]) == L.ERR_INVALID_ARG
+    assert sel(B=2, offs=[0, 5, 4]) == L.ERR_INVALID_ARG
+    assert sel(B=2, offs=[0, 4, 7]) == L.ERR_INVALID_ARG          # offs[B] != T
+    assert sel(B=1, offs=[0, 1100], T=1100) == L.ERR_UNSUPPORTED  # tree too large
+    assert sel(elig=None) == L.ERR_INVALID_ARG
+    assert sel(depth=None) == L.ERR_INVALID_ARG
+    rc, msg = status_and_msg(sel())                               # workspace missing
+    assert rc == L.ERR_WORKSPACE and "workspace" in msg
+    assert sel(ws=FAKE, wsb=16) == L.ERR_WORKSPACE
+    assert sel(ws=V(0x100010), wsb=1 << 20) == L.ERR_WORKSPACE    # misaligned workspace
+    assert sel(T=0, B=0) == L.OK
+
+
+def test_pack_rejects():
+    f = L.lib().acceptmoe_pack_expert_weights
+    assert f(FAKE, L.BF16, 2, 24, 64, V(0x900000), None) == L.ERR_UNSUPPORTED     # N % 16
+    assert f(FAKE, L.BF16, 2, 32, 48, V(0x900000), None) == L.ERR_UNSUPPORTED     # K % 32
+    assert f(FAKE, L.F32, 2, 32, 40, V(0x900000), None) == L.ERR_UNSUPPORTED      # K % 16
+    assert f(FAKE, 3, 2, 32, 64, V(0x900000), None) == L.ERR_INVALID_ARG
+    assert f(None, L.BF16, 2, 32, 64, FAKE, None) == L.ERR_INVALID_ARG
+    assert f(FAKE, L.BF16, 2, 32, 64, V(0x100000 + 4096), None) == L.ERR_INVALID_ARG  # overlap
+    assert f(FAKE, L.BF16, 0, 32, 64, V(0x900000), None) == L.ERR_INVALID_ARG
+
+
+def fwd(**kw):
+    a = dict(h=FAKE, dt=L.BF16, wg=FAKE, wu=FAKE, wd=FAKE, T=8, H=256, I=128, E=16, k=2, idx=FAKE,
+             gate=FAKE, out=FAKE, ws=None, wsb=0)
+    a.update(kw)
+    return L.lib().acceptmoe_moe_forward(a["h"], a["dt"], a["wg"], a["wu"], a["wd"], a["T"], a["H"], a["I"],
+                                         a["E"], a["k"], a["idx"], a["gate"], a["out"], a["ws"], a["wsb"],
+                                         None)
+
+
+def test_forward_rejects():
+    assert fwd(dt=5) == L.ERR_INVALID_ARG
+    assert fwd(H=240) == L.ERR_UNSUPPORTED                 # bf16 needs H % 32
+    assert fwd(I=80) == L.ERR_UNSUPPORTED
+    assert fwd(dt=L.F32, H=248) == L.ERR_UNSUPPORTED       # fp32 needs H % 16
+    assert fwd(E=0) == L.ERR_UNSUPPORTED
+    assert fwd(k=40) == L.ERR_UNSUPPORTED
+    assert fwd(T=-1) == L.ERR_INVALID_ARG
+    assert fwd(out=None) == L.ERR_INVALID_ARG
+    assert fwd(h=V(0x100008)) == L.ERR_INVALID_ARG         # misaligned
+    assert fwd() == L.ERR_WORKSPACE
+    assert fwd(T=0, h=None, out=None) == L.OK

@@ -1,0 +1,345 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.
+
+* route: normwise max-relative error <= 1e-5 against the fp64 product
+* select: given the same fp32 logits, eligible sets, restricted indices and
+  statistics bit-exact; gates within one fp32 rounding
+* forward: normwise max-relative error <= 1e-4 (fp32) / 2e-2 (bf16) against
+  the fp64 grouped oracle (full outputs, or sampled rows at the largest size)
+* end to end (route -> select -> forward): as above, with the oracle routing
+  its own fp64 logits
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import acceptmoe_oracle as O
+from paper_2608_02989_amd import _lib as L
+from paper_2608_02989_amd import ops
+from paper_2608_02989_amd import workload as W
+
+from _util import (FWD_TOL, GATE_RTOL, LOGIT_TOL, HostExperts, hidden_for, normwise_rel,
+                   oracle_logits32)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def to_dev_hidden(cfg, arr):
+    if cfg.dtype == "bf16":
+        return torch.from_numpy(arr.view(np.int16)).view(torch.bfloat16).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).to(DEV)
+
+
+def i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(DEV)
+
+
+def f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(DEV)
+
+
+def u8(a):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a, np.uint8)).to(DEV)
+
+
+# ---------------------------------------------------------------------------
+# route
+# ---------------------------------------------------------------------------
+ROUTE_CASES = [("fp32_small", None, None), ("qwen3_30b_a3b", None, None), ("wide_offload", None, None),
+               ("batched_8x64", None, None), ("qwen3_30b_a3b", 37, 100)]
+
+
+@pytest.mark.parametrize("name,T,E", ROUTE_CASES)
+def test_route_parity(gpu, name, T, E):
+    cfg = W.CONFIGS[name]
+    if E is not None:
+        cfg = W.LayerConfig(**{**cfg.__dict__, "E": E})
+    blk = W.make_block(cfg, block=3, T=T if T else None, B=1 if T else None)
+    hdev, h64 = hidden_for(cfg, blk.hidden)
+    rw = W.router_weights(cfg)
+    say(f"route {name} T={len(h64)} E={cfg.E} H={cfg.H}")
+    z = ops.route(to_dev_hidden(cfg, hdev), f32(rw)).cpu().numpy()
+    ref = O.route(h64, rw.astype(np.float64))
+    err = normwise_rel(z, ref)
+    assert err <= LOGIT_TOL, err
+    # fixed reduction order: identical on a second call
+    z2 = ops.route(to_dev_hidden(cfg, hdev), f32(rw)).cpu().numpy()
+    assert np.array_equal(z.view(np.uint32), z2.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# select (bit-exact given the same fp32 logits)
+# ---------------------------------------------------------------------------
+def run_select_both(z32, parent, depth, prob, offs, k, beta=0.5, mode=0, budget=0, cap=-1, resident=None,
+                    parent_none=False):
+    par_dev = None if parent_none else i32(parent)
+    got = ops.select(f32(z32), par_dev, i32(depth), f32(prob), offs, k, beta, mode, budget, cap, u8(resident))
+    torch.cuda.synchronize()
+    got = {kk: v.cpu().numpy() for kk, v in got.items()}
+    ref = O.select(z32, None if parent_none else parent, depth, prob, offs, k, beta, mode, resident,
+                   None if cap < 0 else cap, budget)
+    return got, ref
+
+
+def assert_select_equal(got, ref, context=""):
+    amb = ref["ambiguous"]
+    assert not amb.any(), f"oracle reports near-tie decisions {amb} {context}"
+    assert np.array_equal(got["eligible"], ref["eligible"]), context
+    assert np.array_equal(got["idx"], ref["idx"]), context
+    assert np.array_equal(got["stats"].astype(np.int64), ref["stats"]), (got["stats"], ref["stats"], context)
+    np.testing.assert_allclose(got["gate"], ref["gate"], rtol=GATE_RTOL, atol=0, err_msg=context)
+
+
+def block_inputs(cfg, block=0, layer=0, rho=0.9, T=None, B=None):
+    blk = W.make_block(cfg, block=block, layer=layer, rho=rho, T=T, B=B)
+    _, h64 = hidden_for(cfg, blk.hidden)
+    z32 = oracle_logits32(h64, W.router_weights(cfg, layer))
+    return blk, z32
+
+
+SEL_CONFIGS = [
+    ("fp32_small", 0.9, 0), ("fp32_small", 0.0, 1), ("qwen3_30b_a3b", 0.9, 0), ("qwen3_30b_a3b", 0.0, 2),
+    ("qwen3_30b_a3b_x48", 0.9, 5), ("wide_offload", 0.9, 0), ("wide_offload", 0.0, 3),
+    ("batched_8x64", 0.9, 0), ("batched_8x64", 0.0, 4),
+]
+
+
+@pytest.mark.parametrize("name,rho,seed", SEL_CONFIGS)
+def test_select_parity_configs(gpu, name, rho, seed):
+    cfg = W.CONFIGS[name]
+    blk, z32 = block_inputs(cfg, block=seed, rho=rho)
+    say(f"select {name} rho={rho} seed={seed} T={len(z32)} B={len(blk.offsets) - 1}")
+    got, ref = run_select_both(z32, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k,
+                               resident=blk.resident)
+    assert_select_equal(got, ref, name)
+
+
+@pytest.mark.parametrize("E,k,T", [(48, 3, 23), (200, 6, 40), (512, 32, 33), (16, 16, 9), (64, 1, 17),
+                                   (100, 8, 130), (128, 8, 1024)])
+def test_select_parity_shapes(gpu, E, k, T):
+    rng = np.random.default_rng(E * 1000 + k)
+    par, dep, sib = W.make_tree(rng, T, 10)
+    prob = (0.75 ** dep * 0.6 ** sib).astype(np.float32)
+    z32 = (rng.standard_normal((T, E)) * 2).astype(np.float32)
+    res = (rng.random(E) < 0.4).astype(np.uint8)
+    say(f"select shape E={E} k={k} T={T}")
+    for resident in (None, res):
+        got, ref = run_select_both(z32, par, dep, prob, None, k, resident=resident)
+        assert_select_equal(got, ref, f"E={E} k={k} T={T} mask={resident is not None}")
+
+
+@pytest.mark.parametrize("mode,budget", [(L.MODE_ALL_EXPERTS, 0), (L.MODE_FIXED_BUDGET, 24),
+                                         (L.MODE_FIXED_BUDGET, 3), (L.MODE_MOESPEC, 24), (L.MODE_COUNT, 24),
+                                         (L.MODE_COUNT, 200)])
+def test_select_parity_modes(gpu, mode, budget):
+    cfg = W.CONFIGS["wide_offload"]
+    blk, z32 = block_inputs(cfg, block=7, rho=0.5)
+    say(f"select mode={mode} budget={budget}")
+    for resident in (None, blk.resident):
+        got, ref = run_select_both(z32, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, mode=mode,
+                                   budget=budget, resident=resident)
+        assert_select_equal(got, ref, f"mode={mode}")
+
+
+def test_select_parity_masks_and_caps(gpu):
+    cfg = W.CONFIGS["qwen3_30b_a3b"]
+    blk, z32 = block_inputs(cfg, block=11, rho=0.9)
+    E = cfg.E
+    say("select masks and caps")
+    for resident, cap in ((np.ones(E, np.uint8), -1), (np.zeros(E, np.uint8), -1), (np.zeros(E, np.uint8), 2),
+                          (np.zeros(E, np.uint8), 0), (blk.resident, -1)):
+        got, ref = run_select_both(z32, blk.parent, blk.depth, blk.prob, None, cfg.k, resident=resident, cap=cap)
+        assert_select_equal(got, ref, f"cap={cap}")
+
+
+def test_select_parity_beta_and_chain(gpu):
+    rng = np.random.default_rng(5)
+    E, k, T = 64, 4, 20
+    par, dep, _ = W.chain(T)
+    prob = (0.8 ** dep).astype(np.float32)
+    z32 = rng.standard_normal((T, E)).astype(np.float32)
+    say("select chain / beta / no parent")
+    for beta in (0.5, 0.0, 1.0, 2.0):
+        got, ref = run_select_both(z32, par, dep, prob, None, k, beta=beta)
+        assert_select_equal(got, ref, f"beta={beta}")
+    got, ref = run_select_both(z32, par, dep, prob, None, k, parent_none=True)
+    assert_select_equal(got, ref, "parent=None")
+
+
+def test_select_parity_root_only_and_ties(gpu):
+    say("select root-only and all-tie logits")
+    z = np.random.default_rng(0).standard_normal((1, 128)).astype(np.float32)
+    got, ref = run_select_both(z, np.array([-1]), np.array([0]), np.array([0.9], np.float32), None, 8)
+    assert_select_equal(got, ref, "root only")
+    assert got["eligible"].sum() == 8
+    # every logit equal: lowest indices win everywhere
+    T = 12
+    rng = np.random.default_rng(1)
+    par, dep, sib = W.make_tree(rng, T, 4)
+    z = np.zeros((T, 40), np.float32)
+    got, ref = run_select_both(z, par, dep, np.ones(T, np.float32), None, 5)
+    assert_select_equal(got, ref, "ties")
+    assert (got["idx"] == np.arange(5)).all()
+    # signed zeros and repeated values
+    z = rng.integers(-3, 3, size=(T, 40)).astype(np.float32)
+    z[z == 0] = -0.0
+    z[::2, ::3] = 0.0
+    got, ref = run_select_both(z, par, dep, (0.7 ** dep).astype(np.float32), None, 5)
+    assert_select_equal(got, ref, "repeated")
+
+
+def test_select_parity_batch_with_invalid_trees(gpu):
+    rng = np.random.default_rng(9)
+    E, k = 128, 8
+    sizes = [64, 1, 0, 17, 64, 5, 33]
+    pars, deps, probs = [], [], []
+    offs = [0]
+    for s in sizes:
+        par, dep, sib = W.make_tree(rng, s, 8) if s else (np.zeros(0, np.int32),) * 3
+        pars.append(np.where(par < 0, -1, par + offs[-1]))
+        deps.append(dep)
+        probs.append((0.75 ** dep * 0.6 ** sib).astype(np.float32))
+        offs.append(offs[-1] + s)
+    par = np.concatenate(pars).astype(np.int32)
+    dep = np.concatenate(deps).astype(np.int32)
+    prob = np.concatenate(probs).astype(np.float32)
+    T = offs[-1]
+    z32 = rng.standard_normal((T, E)).astype(np.float32)
+    # corrupt: tree 3 bad depth, tree 5 parent into tree 4, tree 6 negative prob
+    dep[offs[3] + 4] += 1
+    par[offs[5] + 2] = offs[4]
+    prob[offs[6] + 7] = -0.5
+    say(f"select batch with invalid trees offs={offs}")
+    got, ref = run_select_both(z32, par, dep, prob, offs, k)
+    codes = got["stats"][:, L.NUM_STATS - 2]
+    assert codes[2] == O.TREE_EMPTY and codes[3] != 0 and codes[5] == O.TREE_BAD_PARENT
+    assert codes[6] == O.TREE_BAD_PROB and codes[0] == 0 and codes[1] == 0
+    assert_select_equal(got, ref, "batch with invalid trees")
+
+
+# ---------------------------------------------------------------------------
+# forward
+# ---------------------------------------------------------------------------
+def forward_case(cfg, idx, gate, blk_hidden, layer=0, E=None):
+    hdev, h64 = hidden_for(cfg, blk_hidden)
+    wg, wu, wd = W.expert_weights_torch(cfg, layer, DEV, E=E)
+    got = ops.moe_forward(to_dev_hidden(cfg, hdev), ops.pack_expert_weights(wg), ops.pack_expert_weights(wu),
+                          ops.pack_expert_weights(wd), i32(idx), f32(gate))
+    torch.cuda.synchronize()
+    return got.cpu().numpy(), h64, (HostExperts(wg), HostExperts(wu), HostExperts(wd))
+
+
+FWD_CONFIGS = [("fp32_small", 0), ("qwen3_30b_a3b", 0), ("qwen3_30b_a3b", 1), ("wide_offload", 0)]
+
+
+@pytest.mark.parametrize("name,seed", FWD_CONFIGS)
+def test_forward_parity_full(gpu, name, seed):
+    cfg = W.CONFIGS[name]
+    blk, z32 = block_inputs(cfg, block=seed)
+    sel = O.select(z32, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, resident=blk.resident)
+    say(f"forward {name} seed={seed} routed={sel['stats'][:, O.ST_ROUTED]}")
+    got, h64, (wg, wu, wd) = forward_case(cfg, sel["idx"], sel["gate"], blk.hidden)
+    ref = O.moe_forward_grouped(h64, wg, wu, wd, sel["idx"], sel["gate"], cfg.dtype)
+    err = normwise_rel(got, ref)
+    assert err <= FWD_TOL[cfg.dtype], err
+
+
+def test_forward_parity_batched_sampled(gpu):
+    cfg = W.CONFIGS["batched_8x64"]
+    blk, z32 = block_inputs(cfg, block=0)
+    sel = O.select(z32, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k)
+    say(f"forward batched_8x64 sampled, routed per tree {sel['stats'][:, O.ST_ROUTED]}")
+    got, h64, (wg, wu, wd) = forward_case(cfg, sel["idx"], sel["gate"], blk.hidden)
+    rows = sorted(set(np.random.default_rng(0).choice(len(h64), 12, replace=False).tolist()) | {0, 511})
+    ref = O.moe_forward_rows(h64, wg, wu, wd, sel["idx"], sel["gate"], rows, cfg.dtype)
+    err = normwise_rel(got[rows], ref)
+    assert err <= FWD_TOL[cfg.dtype], err
+    assert np.isfinite(got).all()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_forward_parity_ragged_and_hot_expert(gpu, dtype):
+    # T not a multiple of 16, E not a multiple of 64, one expert receiving every token
+    cfg = W.LayerConfig("ragged", 90 + (dtype == "f32"), dtype, T=100, B=1, H=256, E=20, k=3, I=96,
+                        depth_max=6, commit_rule="depth_sibling", hidden_std=1.0)
+    rng = np.random.default_rng(3)
+    T = 100
+    h32 = rng.standard_normal((T, cfg.H)).astype(np.float32)
+    others = np.array([e for e in range(cfg.E) if e != 7])
+    # expert 7 gets all 100 tokens (several 64-token passes); the rest distinct per row
+    idx = np.stack([np.concatenate([[7], rng.permutation(others)[:cfg.k - 1]]) for _ in range(T)])
+    idx = idx.astype(np.int32)
+    idx[5] = [3, -1, 25]                            # invalid entries are skipped
+    idx[6] = [-1, -1, -1]                           # no expert at all -> zero row
+    idx[9] = [4, 11, 4]                             # a repeated expert counts once (first slot)
+    gate = rng.random((T, cfg.k)).astype(np.float32)
+    say(f"forward ragged dtype={dtype}")
+    got, h64, (wg, wu, wd) = forward_case(cfg, idx, gate, h32)
+    clean = np.where((idx >= 0) & (idx < cfg.E), idx, -1)
+    clean[9, 2] = -1
+    ref = O.moe_forward_grouped(h64, wg, wu, wd, clean, gate, cfg.dtype)
+    err = normwise_rel(got, ref)
+    assert err <= FWD_TOL[cfg.dtype], err
+    assert np.all(got[6] == 0.0)
+
+
+def test_pack_layout_documented(gpu):
+    # fp32 stack whose values encode (e, n, k): check the documented fragment layout
+    E, N, K = 2, 32, 48
+    e_, n_, k_ = np.meshgrid(np.arange(E), np.arange(N), np.arange(K), indexing="ij")
+    src = (e_ * 1e6 + n_ * 1e3 + k_).astype(np.float32)
+    packed = ops.pack_expert_weights(f32(src)).cpu().numpy().reshape(-1, 4)   # 16-B pieces
+    kc_per_row = K * 4 // 64
+    for piece in range(0, packed.shape[0], 7):
+        lane = piece % 64
+        frag = piece // 64
+        kc = frag % kc_per_row
+        nt = (frag // kc_per_row) % (N // 16)
+        e = frag // kc_per_row // (N // 16)
+        row = nt * 16 + lane % 16
+        col = kc * 16 + (lane // 16) * 4
+        assert np.array_equal(packed[piece], src[e, row, col:col + 4]), piece
+
+
+# ---------------------------------------------------------------------------
+# end to end through VerifyLayer (route -> select -> forward)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name,rho", [("fp32_small", 0.9), ("qwen3_30b_a3b", 0.9), ("qwen3_30b_a3b", 0.0),
+                                      ("wide_offload", 0.9)])
+def test_end_to_end(gpu, name, rho):
+    cfg = W.CONFIGS[name]
+    blk = W.make_block(cfg, block=2, rho=rho)
+    hdev, h64 = hidden_for(cfg, blk.hidden)
+    rw = W.router_weights(cfg)
+    wg, wu, wd = W.expert_weights_torch(cfg, 0, DEV)
+    layer = ops.VerifyLayer(f32(rw), wg, wu, wd, cfg.k, max_tokens=cfg.total_tokens, max_trees=cfg.B)
+    say(f"end to end {name} rho={rho}")
+    hd = to_dev_hidden(cfg, hdev)
+    logits, sel, out = layer.step(hd, i32(blk.parent), i32(blk.depth), f32(blk.prob), blk.offsets.tolist(),
+                                  u8(blk.resident))
+    torch.cuda.synchronize()
+    z_gpu = logits.cpu().numpy()
+    z_ref64 = O.route(h64, rw.astype(np.float64))
+    assert normwise_rel(z_gpu, z_ref64) <= LOGIT_TOL
+    ref = O.select(z_ref64.astype(np.float32), blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k,
+                   resident=blk.resident)
+    assert not ref["ambiguous"].any()
+    got_idx = sel["idx"].cpu().numpy()
+    assert np.array_equal(sel["eligible"].cpu().numpy(), ref["eligible"])
+    assert np.array_equal(got_idx, ref["idx"])
+    y_ref = O.moe_forward_grouped(h64, HostExperts(wg), HostExperts(wu), HostExperts(wd), ref["idx"],
+                                  ref["gate"], cfg.dtype)
+    y = out.cpu().numpy()
+    assert normwise_rel(y, y_ref) <= FWD_TOL[cfg.dtype]
+    # determinism: a second step gives bit-identical results
+    logits2, sel2, out2 = layer.step(hd, i32(blk.parent), i32(blk.depth), f32(blk.prob), blk.offsets.tolist(),
+                                     u8(blk.resident))
+    torch.cuda.synchronize()
+    assert np.array_equal(out2.cpu().numpy().view(np.uint32), y.view(np.uint32))
+    assert np.array_equal(sel2["idx"].cpu().numpy(), got_idx)
