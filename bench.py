@@ -41,7 +41,7 @@ def parse():
     ap.add_argument("--blocks", type=int, default=16)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
     ap.add_argument("--no-alt", action="store_true", help="skip the i.i.d. (rho = 0) companion run")
-    ap.add_argument("--graph", action="store_true", help="also time a HIP-graph replay of the step")
+    ap.add_argument("--graph", type=int, default=1, help="time HIP-graph replays of the step sequence (1/0)")
     return ap.parse_args()
 
 
@@ -62,7 +62,7 @@ def main():
     Ttot = cfg.total_tokens
     ebytes = cfg.expert_bytes
     layer_bytes = cfg.E * ebytes
-    n_sets = args.sets or max(2, int(np.ceil(2 * 2**30 / layer_bytes)))
+    n_sets = args.sets or max(4, int(np.ceil(2 * 2**30 / layer_bytes)))
     n_sets = min(n_sets, 16)
     t0 = time.time()
 
@@ -133,6 +133,13 @@ def main():
                     unat[(s, b)] = float(st[:, 5].mean())
         torch.cuda.synchronize()
         seq = combos(warmup + steps)
+        timed = seq[warmup:]
+        r = np.array([routed[c] for c in timed], np.float64)
+        weight_bytes = r * ebytes
+        act_bytes = Ttot * cfg.H * (2 if cfg.dtype == "bf16" else 4) + Ttot * cfg.H * 4 + Ttot * cfg.k * 8
+        fwd_bytes = weight_bytes + act_bytes
+
+        # (1) eager launches, HIP events around every expert-FFN launch
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
         with torch.cuda.stream(stream):
             for (s, b) in seq[:warmup]:
@@ -141,19 +148,41 @@ def main():
             start = torch.cuda.Event(enable_timing=True)
             stop = torch.cuda.Event(enable_timing=True)
             start.record(stream)
-            for i, (s, b) in enumerate(seq[warmup:]):
+            for i, (s, b) in enumerate(timed):
                 run_once(blocks, s, b, stream, evs[i])
             stop.record(stream)
         torch.cuda.synchronize()
-        total_ms = start.elapsed_time(stop)
+        eager_ms = start.elapsed_time(stop)
         fwd_ms = [a.elapsed_time(z) for a, z in evs]
-        timed = seq[warmup:]
-        r = np.array([routed[c] for c in timed], np.float64)
-        weight_bytes = r * ebytes
-        act_bytes = Ttot * cfg.H * (2 if cfg.dtype == "bf16" else 4) + Ttot * cfg.H * 4 + Ttot * cfg.k * 8
-        fwd_bytes = weight_bytes + act_bytes
+
+        # (2) the same step sequence replayed from a HIP graph (no host launch cost)
+        period = n_sets * args.blocks // int(np.gcd(n_sets, args.blocks))
+        graph_ms = None
+        if args.graph:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(stream):
+                with torch.cuda.graph(g, stream=stream):
+                    for (s, b) in combos(period):
+                        run_once(blocks, s, b, stream)
+            torch.cuda.synchronize()
+            reps = max(1, (steps + period - 1) // period)
+            for _ in range(2):
+                g.replay()
+            torch.cuda.synchronize()
+            gs, ge = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            gs.record(stream)
+            with torch.cuda.stream(stream):
+                for _ in range(reps):
+                    g.replay()
+            ge.record(stream)
+            torch.cuda.synchronize()
+            graph_ms = gs.elapsed_time(ge) / (reps * period) * steps
+            del g
+        total_ms = graph_ms if graph_ms is not None else eager_ms
         return dict(
             ms_per_step=total_ms / steps,
+            eager_us=eager_ms / steps * 1e3,
+            graph_us=None if graph_ms is None else graph_ms / steps * 1e3,
             value=float(weight_bytes.sum() / (total_ms * 1e-3) / 1e9),
             fwd_us=float(np.mean(fwd_ms) * 1e3),
             fwd_gbs=float(fwd_bytes.sum() / (np.sum(fwd_ms) * 1e-3) / 1e9),
@@ -165,36 +194,19 @@ def main():
         )
 
     main_m = measure(args.rho, args.steps, args.warmup)
-    log(f"rho={args.rho}: {main_m['ms_per_step'] * 1e3:.1f} us/step, {main_m['value']:.0f} GB/s, "
-        f"ffn {main_m['fwd_us']:.1f} us ({main_m['fwd_gbs']:.0f} GB/s), routed {main_m['routed']:.1f}")
+    log(f"rho={args.rho}: {main_m['ms_per_step'] * 1e3:.1f} us/step (eager {main_m['eager_us']:.1f}), "
+        f"{main_m['value']:.0f} GB/s, ffn {main_m['fwd_us']:.1f} us ({main_m['fwd_gbs']:.0f} GB/s), "
+        f"routed {main_m['routed']:.1f}")
 
     alt = None
     if not args.no_alt and args.rho != 0.0:
         m0 = measure(0.0, args.steps, args.warmup)
         alt = {"rho": 0.0, "value": round(m0["value"], 1), "latency_us": round(m0["ms_per_step"] * 1e3, 2),
+               "eager_latency_us": round(m0["eager_us"], 2),
                "ffn_us": round(m0["fwd_us"], 2), "ffn_gbs": round(m0["fwd_gbs"], 1),
                "routed_experts": round(m0["routed"], 2), "eligible": round(m0["sprime"], 2),
                "natural_union": round(m0["unat"], 2)}
         log(f"rho=0: {m0['ms_per_step'] * 1e3:.1f} us/step, {m0['value']:.0f} GB/s, routed {m0['routed']:.1f}")
-
-    graph_us = None
-    if args.graph:
-        blocks, stream = main_m["blocks"], main_m["stream"]
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.stream(stream):
-            run_once(blocks, 0, 0, stream)
-            torch.cuda.synchronize()
-            with torch.cuda.graph(g, stream=stream):
-                run_once(blocks, 0, 0, stream)
-        torch.cuda.synchronize()
-        st, sp = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        st.record(stream)
-        for _ in range(args.steps):
-            g.replay()
-        sp.record(stream)
-        torch.cuda.synchronize()
-        graph_us = st.elapsed_time(sp) / args.steps * 1e3
-        log(f"graph replay (same weights each step, MALL-warm): {graph_us:.1f} us/step")
 
     # ---- CPU oracle baseline on a bounded sample ----
     cpu = None
@@ -231,7 +243,9 @@ def main():
                      "mfma_util": round(main_m["flops"] / (main_m["fwd_us"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5)},
         "cpu_baseline": cpu,
         "alt_iid": alt,
-        "graph_replay_us": None if graph_us is None else round(graph_us, 2),
+        "timing": "HIP graph replay of the rotated step sequence" if main_m["graph_us"] is not None
+                  else "eager launches",
+        "eager_latency_us": round(main_m["eager_us"], 2),
     }
     print(json.dumps(line), flush=True)
 

@@ -20,7 +20,7 @@ namespace amoe {
 namespace {
 
 constexpr int kDispatchThreads = 1024;
-constexpr int kDispatchChunk = 512;   // tokens per bitmask pass (32 KiB of LDS masks)
+constexpr int kDispatchChunk = kDispatchThreads;  // nodes per bitmask pass (one per thread)
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
@@ -45,37 +45,53 @@ __global__ void pack_kernel(const uint4* __restrict__ src, uint4* __restrict__ d
   }
 }
 
-// Expert served by slot s = t*k + j, or -1 when the slot takes no part in the
-// dispatch: the index lies outside [0, E), or repeats an expert of an earlier
-// slot of the same token (a repeated expert is used once, at its first slot).
-__device__ __forceinline__ int slot_expert(const int32_t* __restrict__ idx, int s, int k, int E) {
-  const int e = idx[s];
-  if (e < 0 || e >= E) return -1;
-  for (int j = (s / k) * k; j < s; ++j)
-    if (idx[j] == e) return -1;
-  return e;
+// A node's routing row, loaded once: experts e[j] and a bit per slot that
+// takes part in the dispatch.  A slot is skipped when its index lies outside
+// [0, E) or repeats the expert of an earlier slot of the same node (a repeated
+// expert is used once, at its first slot).
+template <int KMAX>
+__device__ __forceinline__ uint32_t load_route_row(const int32_t* __restrict__ row, int k, int E,
+                                                   int (&e)[KMAX]) {
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) e[j] = j < k ? row[j] : -1;
+  uint32_t valid = 0u;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    bool ok = (e[j] >= 0) & (e[j] < E);
+#pragma unroll
+    for (int j2 = 0; j2 < j; ++j2) ok = ok & (e[j2] != e[j]);
+    valid |= ok ? (1u << j) : 0u;
+  }
+  return valid;
 }
 
 // ---------------------------------------------------------------------------
-// dispatch: CSR of (expert -> slot ids in node order), active expert list
+// dispatch: CSR of (expert -> slot ids in node order), active expert list.
+// One workgroup; each thread owns one node per pass and keeps its row in
+// registers.  Positions inside an expert's list come from per-expert node
+// bitmasks, so the order is deterministic (node order).
 // ---------------------------------------------------------------------------
+template <int KMAX>
 __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParams p) {
   __shared__ int s_cnt[kMaxExperts];
   __shared__ int s_off[kMaxExperts + 1];
   __shared__ int s_run[kMaxExperts];
   __shared__ uint32_t s_mask[kMaxExperts * (kDispatchChunk / 32)];
-  __shared__ int s_nact;
   const int tid = threadIdx.x;
   const int E = p.E, k = p.k, T = p.T;
-  const int nslot = T * k;
+  constexpr int words = kDispatchChunk / 32;
   for (int e = tid; e < E; e += kDispatchThreads) {
     s_cnt[e] = 0;
     s_run[e] = 0;
   }
   __syncthreads();
-  for (int s = tid; s < nslot; s += kDispatchThreads) {
-    const int e = slot_expert(p.topk_idx, s, k, E);
-    if (e >= 0) atomicAdd(&s_cnt[e], 1);
+  int ev[KMAX];
+  uint32_t valid = 0u;
+  for (int t = tid; t < T; t += kDispatchThreads) {
+    valid = load_route_row<KMAX>(p.topk_idx + static_cast<size_t>(t) * k, k, E, ev);
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j)
+      if (valid & (1u << j)) atomicAdd(&s_cnt[ev[j]], 1);
   }
   __syncthreads();
   if (tid < kWave) {
@@ -97,7 +113,6 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParam
     }
     if (tid == 0) {
       s_off[E] = base;
-      s_nact = abase;
       *p.n_active = abase;
     }
   }
@@ -107,28 +122,29 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParam
     p.off[e] = s_off[e];
   }
   if (tid == 0) p.off[E] = s_off[E];
-  // position of each slot inside its expert list = earlier tokens of that expert
-  const int words = kDispatchChunk / 32;
+  // position of each slot inside its expert list = earlier nodes of that expert
   for (int t0 = 0; t0 < T; t0 += kDispatchChunk) {
-    const int tn = min(kDispatchChunk, T - t0);
+    const int t = t0 + tid;
     for (int i = tid; i < E * words; i += kDispatchThreads) s_mask[i] = 0u;
+    if (t < T && T > kDispatchChunk)
+      valid = load_route_row<KMAX>(p.topk_idx + static_cast<size_t>(t) * k, k, E, ev);
     __syncthreads();
-    for (int i = tid; i < tn * k; i += kDispatchThreads) {
-      const int tl = i / k;
-      const int e = slot_expert(p.topk_idx, (t0 + tl) * k + (i % k), k, E);
-      if (e >= 0) atomicOr(&s_mask[e * words + (tl >> 5)], 1u << (tl & 31));
+    if (t < T) {
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j)
+        if (valid & (1u << j)) atomicOr(&s_mask[ev[j] * words + (tid >> 5)], 1u << (tid & 31));
     }
     __syncthreads();
-    for (int i = tid; i < tn * k; i += kDispatchThreads) {
-      const int tl = i / k;
-      const int s = (t0 + tl) * k + (i % k);
-      const int e = slot_expert(p.topk_idx, s, k, E);
-      if (e >= 0) {
-        const uint32_t* m = s_mask + e * words;
-        int before = 0;
-        for (int w = 0; w < (tl >> 5); ++w) before += __popc(m[w]);
-        before += __popc(m[tl >> 5] & ((1u << (tl & 31)) - 1u));
-        p.ent_slot[s_off[e] + s_run[e] + before] = s;
+    if (t < T) {
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j) {
+        if (valid & (1u << j)) {
+          const uint32_t* m = s_mask + ev[j] * words;
+          int before = 0;
+          for (int w = 0; w < (tid >> 5); ++w) before += __popc(m[w]);
+          before += __popc(m[tid >> 5] & ((1u << (tid & 31)) - 1u));
+          p.ent_slot[s_off[ev[j]] + s_run[ev[j]] + before] = t * k + j;
+        }
       }
     }
     __syncthreads();
@@ -168,172 +184,265 @@ struct F32Path {
 
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
+// k-steps per pipeline stage; two stages are kept in flight
+template <int MT>
+struct Stage {
+  static constexpr int kU = MT <= 2 ? 4 : 2;
+};
+
+// acc[nb][mt] += sum over fragments kc in [kc0, kc1) of x[mt] (A, tokens) times
+// w[nb] (B, weight rows).  w[nb] / x[mt] point at this lane's 16-byte piece of
+// fragment 0; fragment kc sits kc*64 pieces (B) / kc*4 pieces (A) further.
+// Loads run two stages ahead of the MFMAs and carry no branches, so the only
+// waits are the in-order vmcnt waits on the stage being consumed.
+template <class P, int MT, int NB>
+__device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const uint4* const (&x)[MT],
+                                             int kc0, int kc1, floatx4 (&acc)[NB][MT]) {
+  constexpr int kU = Stage<MT>::kU;
+  uint4 wb0[kU][NB], wb1[kU][NB], xb0[kU][MT], xb1[kU][MT];
+  auto load0 = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) wb0[u][nb] = w[nb][static_cast<size_t>(c + u) * kWave];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) xb0[u][mt] = x[mt][(c + u) * 4];
+    }
+  };
+  auto load1 = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) wb1[u][nb] = w[nb][static_cast<size_t>(c + u) * kWave];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) xb1[u][mt] = x[mt][(c + u) * 4];
+    }
+  };
+  auto comp0 = [&]() {
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = P::mma(xb0[u][mt], wb0[u][nb], acc[nb][mt]);
+  };
+  auto comp1 = [&]() {
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = P::mma(xb1[u][mt], wb1[u][nb], acc[nb][mt]);
+  };
+  const int full_end = kc0 + (kc1 - kc0) / kU * kU;
+  if (kc0 < full_end) load0(kc0);
+  for (int c = kc0; c < full_end; c += 2 * kU) {
+    const bool has1 = c + kU < full_end;
+    if (has1) load1(c + kU);
+    comp0();
+    if (has1) {
+      if (c + 2 * kU < full_end) load0(c + 2 * kU);
+      comp1();
+    }
+  }
+  for (int c = full_end; c < kc1; ++c) {
+    uint4 wt[NB], xt[MT];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) wt[nb] = w[nb][static_cast<size_t>(c) * kWave];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) xt[mt] = x[mt][c * 4];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = P::mma(xt[mt], wt[nb], acc[nb][mt]);
+  }
+}
+
 // ---------------------------------------------------------------------------
-// gate/up + SwiGLU.  grid.x = cap_experts * ceil(NT/4), block 256: wave w of
-// workgroup (a, q) owns I-tile nt = 4q + w of active expert a.
+// gate/up + SwiGLU.  One workgroup (4 waves) per (active expert, 16-row tile of
+// I); the waves split the H reduction into 4 contiguous quarters and combine
+// their partial tiles in LDS in a fixed order.  grid.x = cap_experts * (I/16).
 // ---------------------------------------------------------------------------
+constexpr int kGuWaves = 4;
+
 template <class P, int MT>
-__global__ __launch_bounds__(256) void gateup_kernel(ForwardParams p) {
-  const int NT = p.I / 16;
-  const int wg_per_expert = (NT + 3) / 4;
-  const int a = blockIdx.x / wg_per_expert;
-  const int nt = (blockIdx.x % wg_per_expert) * 4 + threadIdx.x / kWave;
-  if (a >= *p.n_active || nt >= NT) return;
-  const int lane = lane_id();
+__device__ __forceinline__ void gateup_pass(const ForwardParams& p, int e, int nt, int n_e, int o_e, int m0,
+                                            floatx4 (*red)[kWave][2][4]) {
+  const int wave = threadIdx.x / kWave, lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
+  const int H = p.H, I = p.I;
+  const int KC = H / P::kKF;
+  const int rowq = H * P::kElemBytes / 16;
+  const int NT = I / 16;
+  const uint4* hid = static_cast<const uint4*>(p.hidden);
+  const int tok0 = p.ent_slot[o_e] / p.k;  // rows past n_e read a valid row; their outputs are dropped
+  const uint4* x[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = m0 + mt * 16 + r;
+    const int tok = m < n_e ? p.ent_slot[o_e + m] / p.k : tok0;
+    x[mt] = hid + static_cast<size_t>(tok) * rowq + g;
+  }
+  const size_t frag0 = (static_cast<size_t>(e) * NT + nt) * KC;
+  const uint4* w[2] = {static_cast<const uint4*>(p.w_gate) + frag0 * kWave + lane,
+                       static_cast<const uint4*>(p.w_up) + frag0 * kWave + lane};
+  floatx4 acc[2][MT];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int kc0 = wave * KC / kGuWaves, kc1 = (wave + 1) * KC / kGuWaves;
+  stream_tiles<P, MT, 2>(w, x, kc0, kc1, acc);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    red[wave][lane][0][mt] = acc[0][mt];
+    red[wave][lane][1][mt] = acc[1][mt];
+  }
+  __syncthreads();
+  // wave w finishes M-tiles w, w+4, ...: fixed-order sum over the 4 K quarters
+  for (int mt = wave; mt < MT; mt += kGuWaves) {
+    floatx4 sg = red[0][lane][0][mt], su = red[0][lane][1][mt];
+#pragma unroll
+    for (int w2 = 1; w2 < kGuWaves; ++w2) {
+      const floatx4 qg = red[w2][lane][0][mt], qu = red[w2][lane][1][mt];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sg[i] += qg[i];
+        su[i] += qu[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + mt * 16 + 4 * g + i;
+      if (m < n_e) {
+        const float v = silu_mul(sg[i], su[i]);
+        const size_t idx = static_cast<size_t>(o_e + m) * I + nt * 16 + r;
+        if (P::kElemBytes == 2)
+          static_cast<uint16_t*>(p.act)[idx] = float_to_bf16_bits(v);
+        else
+          static_cast<float*>(p.act)[idx] = v;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+template <class P, int MTMAX>
+__global__ __launch_bounds__(256) void gateup_kernel(ForwardParams p) {
+  __shared__ floatx4 red[kGuWaves][kWave][2][4];
+  const int NT = p.I / 16;
+  const int a = blockIdx.x / NT;
+  const int nt = blockIdx.x % NT;
+  if (a >= *p.n_active) return;
   const int e = p.active[a];
   const int n_e = p.cnt[e];
   const int o_e = p.off[e];
+  for (int m0 = 0; m0 < n_e; m0 += 16 * MTMAX) {
+    const int nmt = min(MTMAX, (n_e - m0 + 15) / 16);
+    if (nmt == 1) gateup_pass<P, 1>(p, e, nt, n_e, o_e, m0, red);
+    else if (MTMAX >= 2 && nmt == 2) gateup_pass<P, (MTMAX >= 2 ? 2 : 1)>(p, e, nt, n_e, o_e, m0, red);
+    else if (MTMAX >= 3 && nmt == 3) gateup_pass<P, (MTMAX >= 3 ? 3 : 1)>(p, e, nt, n_e, o_e, m0, red);
+    else gateup_pass<P, MTMAX>(p, e, nt, n_e, o_e, m0, red);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// down projection.  Wave w of workgroup (a, q) owns H-tile ht = 4q + w of
+// active expert a over the whole I reduction.  grid.x = cap_experts * ceil(HT/4).
+// ---------------------------------------------------------------------------
+template <class P, int MT>
+__device__ __forceinline__ void down_pass(const ForwardParams& p, int e, int ht, int n_e, int o_e, int m0) {
+  const int lane = lane_id();
+  const int r = lane & 15, g = lane >> 4;
   const int H = p.H, I = p.I;
-  const int KC = H / P::kKF;                 // fragments along K
-  const int rowq = H * P::kElemBytes / 16;   // 16-B pieces per hidden row
-
-  const uint4* hid = static_cast<const uint4*>(p.hidden);
-  const size_t frag0 = (static_cast<size_t>(e) * NT + nt) * KC;
-  const uint4* bg = static_cast<const uint4*>(p.w_gate) + frag0 * kWave + lane;
-  const uint4* bu = static_cast<const uint4*>(p.w_up) + frag0 * kWave + lane;
-
-  for (int m0 = 0; m0 < n_e; m0 += 16 * MT) {
-    const int nmt = min(MT, (n_e - m0 + 15) / 16);
-    const uint4* ap[MT];
-    bool av[MT];
+  const int KC = I / P::kKF;
+  const int rowq = I * P::kElemBytes / 16;
+  const int HT = H / 16;
+  const uint4* act = static_cast<const uint4*>(p.act);
+  const uint4* x[MT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = m0 + mt * 16 + r;
-      av[mt] = (mt < nmt) && (m < n_e);
-      const int tok = av[mt] ? p.ent_slot[o_e + m] / p.k : 0;
-      ap[mt] = hid + static_cast<size_t>(tok) * rowq + g;
-    }
-    floatx4 accg[MT], accu[MT];
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = m0 + mt * 16 + r;
+    x[mt] = act + static_cast<size_t>(o_e + (m < n_e ? m : 0)) * rowq + g;
+  }
+  const size_t frag0 = (static_cast<size_t>(e) * HT + ht) * KC;
+  const uint4* w[1] = {static_cast<const uint4*>(p.w_down) + frag0 * kWave + lane};
+  floatx4 acc[1][MT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      accg[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      accu[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
-#pragma unroll 4
-    for (int kc = 0; kc < KC; ++kc) {
-      const uint4 wg = bg[static_cast<size_t>(kc) * kWave];
-      const uint4 wu = bu[static_cast<size_t>(kc) * kWave];
+  for (int mt = 0; mt < MT; ++mt) acc[0][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  stream_tiles<P, MT, 1>(w, x, 0, KC, acc);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        if (mt < nmt) {
-          const uint4 x = av[mt] ? ap[mt][kc * 4] : make_uint4(0u, 0u, 0u, 0u);
-          accg[mt] = P::mma(x, wg, accg[mt]);
-          accu[mt] = P::mma(x, wu, accu[mt]);
-        }
-      }
-    }
-    // epilogue: act[o_e + m][nt*16 + r] for rows m = m0 + mt*16 + 4g + i
+  for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      if (mt >= nmt) continue;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = m0 + mt * 16 + 4 * g + i;
-        if (m < n_e) {
-          const float v = silu_mul(accg[mt][i], accu[mt][i]);
-          const size_t idx = static_cast<size_t>(o_e + m) * I + nt * 16 + r;
-          if (P::kElemBytes == 2)
-            static_cast<uint16_t*>(p.act)[idx] = float_to_bf16_bits(v);
-          else
-            static_cast<float*>(p.act)[idx] = v;
-        }
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + mt * 16 + 4 * g + i;
+      if (m < n_e) {
+        const int s = p.ent_slot[o_e + m];
+        p.ys[static_cast<size_t>(s) * H + ht * 16 + r] = p.topk_gate[s] * acc[0][mt][i];
       }
     }
   }
 }
 
-// ---------------------------------------------------------------------------
-// down projection.  grid.x = cap_experts * ceil(HT/4); wave w of workgroup
-// (a, q) owns H-tile ht = 4q + w of active expert a.
-// ---------------------------------------------------------------------------
-template <class P, int MT>
+template <class P, int MTMAX>
 __global__ __launch_bounds__(256) void down_kernel(ForwardParams p) {
   const int HT = p.H / 16;
   const int wg_per_expert = (HT + 3) / 4;
   const int a = blockIdx.x / wg_per_expert;
   const int ht = (blockIdx.x % wg_per_expert) * 4 + threadIdx.x / kWave;
   if (a >= *p.n_active || ht >= HT) return;
-  const int lane = lane_id();
-  const int r = lane & 15, g = lane >> 4;
   const int e = p.active[a];
   const int n_e = p.cnt[e];
   const int o_e = p.off[e];
-  const int H = p.H, I = p.I;
-  const int KC = I / P::kKF;
-  const int rowq = I * P::kElemBytes / 16;
-
-  const uint4* act = static_cast<const uint4*>(p.act);
-  const size_t frag0 = (static_cast<size_t>(e) * HT + ht) * KC;
-  const uint4* bd = static_cast<const uint4*>(p.w_down) + frag0 * kWave + lane;
-
-  for (int m0 = 0; m0 < n_e; m0 += 16 * MT) {
-    const int nmt = min(MT, (n_e - m0 + 15) / 16);
-    const uint4* ap[MT];
-    bool av[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = m0 + mt * 16 + r;
-      av[mt] = (mt < nmt) && (m < n_e);
-      ap[mt] = act + static_cast<size_t>(av[mt] ? o_e + m : 0) * rowq + g;
-    }
-    floatx4 acc[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-    for (int kc = 0; kc < KC; ++kc) {
-      const uint4 w = bd[static_cast<size_t>(kc) * kWave];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        if (mt < nmt) {
-          const uint4 x = av[mt] ? ap[mt][kc * 4] : make_uint4(0u, 0u, 0u, 0u);
-          acc[mt] = P::mma(x, w, acc[mt]);
-        }
-      }
-    }
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      if (mt >= nmt) continue;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = m0 + mt * 16 + 4 * g + i;
-        if (m < n_e) {
-          const int s = p.ent_slot[o_e + m];
-          p.ys[static_cast<size_t>(s) * H + ht * 16 + r] = p.topk_gate[s] * acc[mt][i];
-        }
-      }
-    }
+  for (int m0 = 0; m0 < n_e; m0 += 16 * MTMAX) {
+    const int nmt = min(MTMAX, (n_e - m0 + 15) / 16);
+    if (nmt == 1) down_pass<P, 1>(p, e, ht, n_e, o_e, m0);
+    else if (MTMAX >= 2 && nmt == 2) down_pass<P, (MTMAX >= 2 ? 2 : 1)>(p, e, ht, n_e, o_e, m0);
+    else if (MTMAX >= 3 && nmt == 3) down_pass<P, (MTMAX >= 3 ? 3 : 1)>(p, e, ht, n_e, o_e, m0);
+    else down_pass<P, MTMAX>(p, e, ht, n_e, o_e, m0);
   }
 }
 
 // ---------------------------------------------------------------------------
-// combine: out[t, h] = sum_j ys[t*k + j, h] over valid slots, slot order
+// combine: out[t, h] = sum over the dispatched slots of token t, in slot order.
+// The routing row and all k expert rows are loaded before any is used (rows
+// of skipped slots are read but discarded).
 // ---------------------------------------------------------------------------
+template <int KMAX>
 __global__ __launch_bounds__(256) void combine_kernel(ForwardParams p) {
   const int t = blockIdx.y;
   const int h4 = blockIdx.x * blockDim.x + threadIdx.x;  // float4 column
   const int H = p.H, k = p.k;
   if (h4 * 4 >= H) return;
+  int ev[KMAX];
+  const uint32_t valid = load_route_row<KMAX>(p.topk_idx + static_cast<size_t>(t) * k, k, p.E, ev);
+  float4 v[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    const int jj = j < k ? j : k - 1;
+    v[j] = reinterpret_cast<const float4*>(p.ys + (static_cast<size_t>(t) * k + jj) * H)[h4];
+  }
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int j = 0; j < k; ++j) {
-    if (slot_expert(p.topk_idx, t * k + j, k, p.E) < 0) continue;
-    const float4 v = reinterpret_cast<const float4*>(p.ys + static_cast<size_t>(t * k + j) * H)[h4];
-    s.x += v.x;
-    s.y += v.y;
-    s.z += v.z;
-    s.w += v.w;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (valid & (1u << j)) {
+      s.x += v[j].x;
+      s.y += v[j].y;
+      s.z += v[j].z;
+      s.w += v[j].w;
+    }
   }
   reinterpret_cast<float4*>(p.out + static_cast<size_t>(t) * H)[h4] = s;
 }
 
-template <class P, int MT>
+template <class P, int MTMAX>
 hipError_t launch_ffn(const ForwardParams& p, int cap, hipStream_t stream) {
-  const int gu_wg = (p.I / 16 + 3) / 4;
+  const int gu_wg = p.I / 16;
   const int dn_wg = (p.H / 16 + 3) / 4;
-  gateup_kernel<P, MT><<<dim3(cap * gu_wg), 256, 0, stream>>>(p);
+  gateup_kernel<P, MTMAX><<<dim3(cap * gu_wg), 256, 0, stream>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  down_kernel<P, MT><<<dim3(cap * dn_wg), 256, 0, stream>>>(p);
+  down_kernel<P, MTMAX><<<dim3(cap * dn_wg), 256, 0, stream>>>(p);
   return hipGetLastError();
 }
 
@@ -375,7 +484,11 @@ void forward_carve(void* ws, ForwardParams& p) {
 }
 
 hipError_t launch_forward(const ForwardParams& p, hipStream_t stream) {
-  dispatch_kernel<<<1, kDispatchThreads, 0, stream>>>(p);
+  const bool small_k = p.k <= 8;
+  if (small_k)
+    dispatch_kernel<8><<<1, kDispatchThreads, 0, stream>>>(p);
+  else
+    dispatch_kernel<kMaxTopK><<<1, kDispatchThreads, 0, stream>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   // upper bound on active experts: min(E, T*k)
@@ -387,7 +500,10 @@ hipError_t launch_forward(const ForwardParams& p, hipStream_t stream) {
   }
   if (err != hipSuccess) return err;
   dim3 cgrid((p.H / 4 + 255) / 256, p.T);
-  combine_kernel<<<cgrid, 256, 0, stream>>>(p);
+  if (small_k)
+    combine_kernel<8><<<cgrid, 256, 0, stream>>>(p);
+  else
+    combine_kernel<kMaxTopK><<<cgrid, 256, 0, stream>>>(p);
   return hipGetLastError();
 }
 

@@ -34,9 +34,10 @@ struct SelectParams {
   int32_t* topk_idx;
   float* topk_gate;
   int32_t* stats;
-  int32_t* ws_kidx;   // [T, k] natural top-k (slot order)
-  double* ws_contrib; // [T, k] alpha_t * r_{t,e}
-  double* ws_rfull;   // [T, E] full softmax rows (MoE-Spec mass only)
+  int32_t* ws_kidx;    // [T, k] natural top-k experts (slot order)
+  double* ws_r;        // [T, k] their router probabilities r_{t,e} (fp64)
+  double* ws_rfull;    // [T, E] full softmax rows (MoE-Spec mass only)
+  uint32_t* ws_routed; // [B, kMaxExperts / 32] experts that received a node of tree b
   double beta;
   int T, E, k, B, mode, budget, removal_cap;
 };

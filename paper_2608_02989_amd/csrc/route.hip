@@ -1,7 +1,8 @@
 // Router logits z_t = W_r h_t (Sec. 3.1): an fp32 [T,H] x [E,H]^T product on
 // the fp32 MFMA (v_mfma_f32_16x16x4f32), one 16-token x 16-expert tile per
-// workgroup, the H reduction split over the 4 waves and combined in LDS in a
-// fixed order (deterministic).
+// workgroup of 16 waves.  Each wave reduces a contiguous slice of H with
+// branch-free loads (rows past T / E are clamped, computed and dropped), and
+// the 16 partial tiles are summed in LDS in a fixed order (deterministic).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -9,7 +10,7 @@ namespace amoe {
 
 namespace {
 
-constexpr int kRouteWaves = 4;
+constexpr int kRouteWaves = 16;
 
 __device__ __forceinline__ float4 load4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 
@@ -19,30 +20,29 @@ __device__ __forceinline__ float4 load4(const uint16_t* p) {
                      __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
 }
 
-// grid (ceil(E/16), ceil(T/16)), block 256.  Lane (r, g): token row t0 + r of
+// grid (ceil(E/16), ceil(T/16)), block 1024.  Lane (r, g): token row t0 + r of
 // the A tile and expert column e0 + r of the B tile; K slice g of each
 // 16-wide chunk is the float4 at offset 4g, component j feeds MFMA j.
 template <typename TIn>
-__global__ __launch_bounds__(256) void route_kernel(const TIn* __restrict__ hidden,
-                                                    const float* __restrict__ w, int T, int H, int E,
-                                                    float* __restrict__ logits) {
+__global__ __launch_bounds__(kRouteWaves * kWave) void route_kernel(const TIn* __restrict__ hidden,
+                                                                   const float* __restrict__ w, int T, int H,
+                                                                   int E, float* __restrict__ logits) {
   __shared__ floatx4 part[kRouteWaves][kWave];
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
   const int e0 = blockIdx.x * 16, t0 = blockIdx.y * 16;
-  const int t = t0 + r, e = e0 + r;
-  const bool tv = t < T, ev = e < E;
-  const TIn* hrow = hidden + static_cast<size_t>(tv ? t : 0) * H + 4 * g;
-  const float* wrow = w + static_cast<size_t>(ev ? e : 0) * H + 4 * g;
+  const int t = min(t0 + r, T - 1), e = min(e0 + r, E - 1);
+  const TIn* hrow = hidden + static_cast<size_t>(t) * H + 4 * g;
+  const float* wrow = w + static_cast<size_t>(e) * H + 4 * g;
 
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
   const int nchunk = H / 16;
-#pragma unroll 4
-  for (int c = wave; c < nchunk; c += kRouteWaves) {
-    const int k0 = c * 16;
-    float4 a = tv ? load4(hrow + k0) : make_float4(0.f, 0.f, 0.f, 0.f);
-    float4 b = ev ? load4(wrow + k0) : make_float4(0.f, 0.f, 0.f, 0.f);
+  const int c0 = wave * nchunk / kRouteWaves, c1 = (wave + 1) * nchunk / kRouteWaves;
+#pragma unroll 8
+  for (int c = c0; c < c1; ++c) {
+    const float4 a = load4(hrow + c * 16);
+    const float4 b = load4(wrow + c * 16);
     acc = mfma_f32_16x16x4(a.x, b.x, acc);
     acc = mfma_f32_16x16x4(a.y, b.y, acc);
     acc = mfma_f32_16x16x4(a.z, b.z, acc);
@@ -54,17 +54,17 @@ __global__ __launch_bounds__(256) void route_kernel(const TIn* __restrict__ hidd
     floatx4 s = part[0][lane];
 #pragma unroll
     for (int w2 = 1; w2 < kRouteWaves; ++w2) {
-      floatx4 q = part[w2][lane];
+      const floatx4 q = part[w2][lane];
       s[0] += q[0];
       s[1] += q[1];
       s[2] += q[2];
       s[3] += q[3];
     }
-    if (ev) {
+    if (e0 + r < E) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int tt = t0 + 4 * g + i;
-        if (tt < T) logits[static_cast<size_t>(tt) * E + e] = s[i];
+        if (tt < T) logits[static_cast<size_t>(tt) * E + e0 + r] = s[i];
       }
     }
   }
@@ -75,12 +75,13 @@ __global__ __launch_bounds__(256) void route_kernel(const TIn* __restrict__ hidd
 hipError_t launch_route(const void* hidden, int hidden_is_bf16, const float* router_w, int T, int H,
                         int E, float* logits, hipStream_t stream) {
   dim3 grid((E + 15) / 16, (T + 15) / 16);
+  const int block = kRouteWaves * kWave;
   if (hidden_is_bf16)
-    route_kernel<uint16_t><<<grid, 256, 0, stream>>>(static_cast<const uint16_t*>(hidden), router_w,
-                                                     T, H, E, logits);
+    route_kernel<uint16_t><<<grid, block, 0, stream>>>(static_cast<const uint16_t*>(hidden), router_w, T, H,
+                                                       E, logits);
   else
-    route_kernel<float><<<grid, 256, 0, stream>>>(static_cast<const float*>(hidden), router_w, T, H,
-                                                  E, logits);
+    route_kernel<float><<<grid, block, 0, stream>>>(static_cast<const float*>(hidden), router_w, T, H, E,
+                                                    logits);
   return hipGetLastError();
 }
 

@@ -1,16 +1,17 @@
-// AcceptMoE eligible-set selection, one 1024-thread workgroup per draft tree.
+// AcceptMoE eligible-set selection as three kernels.
 //
-// Phases (each separated by a workgroup barrier):
-//   P1  tree checks and depth counts N_d                          (Sec. 3.1, 3.2)
-//   P2  per node (one wave per node): natural top-k K_t over the fp32
-//       logits, r_t = softmax(z_t) in fp64, alpha_t r_{t,e} for e in K_t,
-//       votes v_e and the root anchor                  (Sec. 3.1 Eq. 1, Eq. 3, Eq. 5)
-//   P3  utility u_e = sum_t alpha_t r_{t,e} 1[e in K_t], summed in node order
-//       through a dense LDS tile                                  (Eq. 4)
-//   P4  effective rank over R = [E] \ A, self-sized set S, optional
-//       residency pruning -> S'                       (Eq. 6, Sec. 3.3, Eq. 7)
-//   P5  per node: restricted top-k over S' and renormalised gates  (Eq. 2)
-//   P6  eligible mask and per-tree statistics
+//   natural_kernel    one wave per node, spread over many CUs: natural top-k
+//                     K_t over the fp32 logits and r_t = softmax(z_t) in fp64
+//                     for the selected experts                  (Sec. 3.1, Eq. 1)
+//   tree_kernel       one 1024-thread workgroup per draft tree:
+//     P1  depth / parent / probability of every node; tree checks, depth
+//         counts N_d, importance alpha_t = p_t^beta / sqrt(N_{d_t})   (Eq. 3)
+//     P3  utility u_e = sum_t alpha_t r_{t,e} 1[e in K_t], summed in node order
+//         through a dense LDS tile; votes v_e; root anchor A         (Eq. 4, Eq. 5)
+//     P4  effective rank over R = [E] \ A, self-sized set S, optional
+//         residency pruning -> S'                        (Eq. 6, Sec. 3.3, Eq. 7)
+//   restricted_kernel one wave per node: restricted top-k over S' and
+//                     renormalised gates                                  (Eq. 2)
 //
 // Top-k is a wave-wide radix select on order-preserving 32-bit keys: the k-th
 // largest key is found bit by bit with ballots, keys above it are taken,
@@ -24,8 +25,9 @@ namespace amoe {
 namespace {
 
 constexpr int kSelThreads = 1024;
-constexpr int kSelWaves = kSelThreads / kWave;
+constexpr int kNodeWaves = 4;        // nodes per workgroup in the per-node kernels
 constexpr int kDenseDoubles = 4096;  // P3 LDS tile: chunk_tokens * E <= this
+constexpr int kRoutedWords = kMaxExperts / 32;
 
 enum { MODE_SELF = 0, MODE_ALL = 1, MODE_FIXED = 2, MODE_MOESPEC = 3, MODE_COUNT = 4 };
 enum { CODE_OK = 0, CODE_EMPTY = 1, CODE_ROOT = 2, CODE_PARENT = 3, CODE_DEPTH = 4, CODE_PROB = 5 };
@@ -34,22 +36,30 @@ struct SelShared {
   int code;
   int n_anchor, n_unat, n_R, n_pos, n_S, n_C, n_Sp, n_routed;
   int n_er, n_take, budget_a, m_star;
-  double Z, Hsum;
-  int Nd[kMaxTreeNodes];
-  int votes[kMaxExperts];
-  int rankv[kMaxExperts];
-  int pv[kMaxExperts];
-  double u[kMaxExperts];
-  double dense[kDenseDoubles];
-  uint8_t anchor[kMaxExperts];
-  uint8_t inS[kMaxExperts];
-  uint8_t inSp[kMaxExperts];
-  uint8_t routed[kMaxExperts];
-  uint8_t resident[kMaxExperts];
-  // per-wave compaction scratch for top-k slot ordering
-  uint32_t sk[kSelWaves][kMaxTopK];
-  int se[kSelWaves][kMaxTopK];
-  float sz[kSelWaves][kMaxTopK];
+  double Z;
+  alignas(16) int Nd[kMaxTreeNodes];
+  alignas(16) double alpha[kMaxTreeNodes];
+  alignas(16) int votes[kMaxExperts];
+  alignas(16) int rankv[kMaxExperts];
+  alignas(16) int pv[kMaxExperts];
+  alignas(16) double u[kMaxExperts];
+  alignas(16) double score[kMaxExperts];
+  alignas(16) double dense[kDenseDoubles];
+  // per-expert flags (entries E..kMaxExperts-1 stay 0)
+  alignas(16) uint8_t anchor[kMaxExperts];
+  alignas(16) uint8_t inR[kMaxExperts];
+  alignas(16) uint8_t inS[kMaxExperts];
+  alignas(16) uint8_t inC[kMaxExperts];
+  alignas(16) uint8_t inSp[kMaxExperts];
+  alignas(16) uint8_t routed[kMaxExperts];
+  alignas(16) uint8_t resident[kMaxExperts];
+};
+
+// per-wave compaction scratch for top-k slot ordering
+struct NodeScratch {
+  alignas(16) uint32_t sk[kNodeWaves][kMaxTopK];
+  alignas(16) int se[kNodeWaves][kMaxTopK];
+  alignas(16) float sz[kNodeWaves][kMaxTopK];
 };
 
 // k-th largest key among the wave's EPL*64 keys (0 if fewer than k are non-zero).
@@ -83,7 +93,7 @@ __device__ __forceinline__ int wave_topk_compact(const uint32_t (&key)[EPL], con
   for (int i = 0; i < EPL; ++i) {
     const bool eq = (key[i] == thr) && (key[i] != 0u);
     const uint64_t eqm = __ballot(eq);
-    const bool sel = (key[i] > thr) || (eq && (eq_before + popc64(eqm & below)) < need);
+    const bool sel = (key[i] > thr) | (eq & ((eq_before + popc64(eqm & below)) < need));
     eq_before += popc64(eqm);
     const uint64_t sm = __ballot(sel);
     if (sel) {
@@ -99,12 +109,54 @@ __device__ __forceinline__ int wave_topk_compact(const uint32_t (&key)[EPL], con
 }
 
 // Slot (rank) of compacted entry j among the n selected: (key desc, index asc).
+// Reads the scratch four entries at a time.
 __device__ __forceinline__ int slot_of(int j, int n, const uint32_t* sk, const int* se) {
   const uint32_t kj = sk[j];
   const int ej = se[j];
   int r = 0;
-  for (int i = 0; i < n; ++i) r += (sk[i] > kj) || (sk[i] == kj && se[i] < ej);
+  for (int i0 = 0; i0 < n; i0 += 4) {
+    const uint4 kk = *reinterpret_cast<const uint4*>(sk + i0);
+    const int4 ee = *reinterpret_cast<const int4*>(se + i0);
+    // bitwise (not short-circuit) logic keeps this branch-free
+    r += static_cast<int>((i0 + 0 < n) & ((kk.x > kj) | ((kk.x == kj) & (ee.x < ej))));
+    r += static_cast<int>((i0 + 1 < n) & ((kk.y > kj) | ((kk.y == kj) & (ee.y < ej))));
+    r += static_cast<int>((i0 + 2 < n) & ((kk.z > kj) | ((kk.z == kj) & (ee.z < ej))));
+    r += static_cast<int>((i0 + 3 < n) & ((kk.w > kj) | ((kk.w == kj) & (ee.w < ej))));
+  }
   return r;
+}
+
+// rank[e] for every flagged e (entries of unflagged experts are left at 0):
+// the E x E comparison is split over all threads of the workgroup, each thread
+// counting one slice of competitors for one expert; integer partial counts
+// are added with LDS atomics (order-independent).  rank must be zeroed first.
+template <bool kDesc>
+__device__ __forceinline__ void rank_all(const double* v, const uint8_t* flag, int E, int* rank, int tid) {
+  const int parts = E <= 128 ? 8 : (E <= 256 ? 4 : 2);
+  const int span = ((E + parts - 1) / parts + 7) & ~7;  // competitors per slice, multiple of 8
+  for (int item = tid; item < E * parts; item += kSelThreads) {
+    const int e = item / parts, part = item % parts;
+    if (!flag[e]) continue;
+    const double ve = v[e];
+    const int j_begin = part * span;
+    const int j_end = min(E, j_begin + span);
+    int r = 0;
+    for (int j0 = j_begin; j0 < j_end; j0 += 8) {
+      const double2 a = *reinterpret_cast<const double2*>(v + j0);
+      const double2 b = *reinterpret_cast<const double2*>(v + j0 + 2);
+      const double2 c = *reinterpret_cast<const double2*>(v + j0 + 4);
+      const double2 d = *reinterpret_cast<const double2*>(v + j0 + 6);
+      const uint2 f = *reinterpret_cast<const uint2*>(flag + j0);
+      const double vv[8] = {a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const bool fl = ((q < 4 ? f.x >> (8 * q) : f.y >> (8 * (q - 4))) & 0xffu) != 0u;
+        const bool beats = kDesc ? (vv[q] > ve) : (vv[q] < ve);
+        r += static_cast<int>(fl & (beats | ((vv[q] == ve) & (j0 + q < e))));
+      }
+    }
+    if (r) atomicAdd(&rank[e], r);
+  }
 }
 
 // Deterministic workgroup sum of one double per expert (E <= 512): wave 0
@@ -116,8 +168,79 @@ __device__ __forceinline__ double wg_sum_experts(const double* vals, int E, int 
   return wave == 0 ? wave_sum_f64(s) : 0.0;
 }
 
+// Workgroup counters without contention: each wave adds its ballot count (or
+// its lane sum) with a single LDS atomic.  Integer sums, so the order of the
+// atomics does not change the result.
+__device__ __forceinline__ void wg_count(bool pred, int* counter, int lane) {
+  const int c = popc64(__ballot(pred));
+  if (lane == 0 && c) atomicAdd(counter, c);
+}
+
+__device__ __forceinline__ void wg_add(int v, int* counter, int lane) {
+  const int s = wave_sum_i32(v);
+  if (lane == 0 && s) atomicAdd(counter, s);
+}
+
 template <int EPL>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, TreeOffsets offs) {
+__device__ __forceinline__ void load_row(const float* __restrict__ zrow, int E, int lane, float (&zv)[EPL]) {
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + kWave * i;
+    zv[i] = e < E ? zrow[e] : -INFINITY;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// natural top-k and router probabilities, one wave per node
+// ---------------------------------------------------------------------------
+template <int EPL>
+__global__ __launch_bounds__(kNodeWaves * kWave) void natural_kernel(SelectParams p) {
+  __shared__ NodeScratch ns;
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int t = blockIdx.x * kNodeWaves + wave;
+  if (t >= p.T) return;
+  const int E = p.E, k = p.k;
+  float zv[EPL];
+  uint32_t key[EPL];
+  load_row<EPL>(p.logits + static_cast<size_t>(t) * E, E, lane, zv);
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) key[i] = (lane + kWave * i) < E ? logit_key(zv[i]) : 0u;
+  // softmax over all E in fp64 (max subtracted)
+  float zmax = zv[0];
+#pragma unroll
+  for (int i = 1; i < EPL; ++i) zmax = fmaxf(zmax, zv[i]);
+  zmax = wave_max_f32(zmax);
+  double ex[EPL];
+  double den = 0.0;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    ex[i] = (lane + kWave * i) < E ? exp(static_cast<double>(zv[i]) - static_cast<double>(zmax)) : 0.0;
+    den += ex[i];
+  }
+  den = wave_sum_f64(den);
+  if (p.mode == MODE_MOESPEC) {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = lane + kWave * i;
+      if (e < E) p.ws_rfull[static_cast<size_t>(t) * E + e] = ex[i] / den;
+    }
+  }
+  uint32_t* sk = ns.sk[wave];
+  int* se = ns.se[wave];
+  float* sz = ns.sz[wave];
+  const int n = wave_topk_compact<EPL>(key, zv, k, lane, sk, se, sz);
+  if (lane < n) {
+    const int slot = slot_of(lane, n, sk, se);
+    p.ws_kidx[static_cast<size_t>(t) * k + slot] = se[lane];
+    p.ws_r[static_cast<size_t>(t) * k + slot] =
+        exp(static_cast<double>(sz[lane]) - static_cast<double>(zmax)) / den;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// eligible set of one tree
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeOffsets offs) {
   __shared__ SelShared sh;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = lane_id();
@@ -127,49 +250,48 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Tre
   const int E = p.E, k = p.k;
   const bool has_mask = p.resident != nullptr;
 
-  // ---------------- P1: tree checks, N_d ----------------
+  // ---------------- P1: inputs, tree checks, N_d ----------------
   if (tid == 0) {
     sh.code = Tb > 0 ? 0x7fffffff : CODE_EMPTY;
     sh.n_anchor = sh.n_unat = sh.n_R = sh.n_pos = sh.n_S = sh.n_C = sh.n_Sp = sh.n_routed = 0;
     sh.budget_a = sh.m_star = sh.n_er = sh.n_take = 0;
   }
   for (int i = tid; i < kMaxTreeNodes; i += kSelThreads) sh.Nd[i] = 0;
-  for (int e = tid; e < E; e += kSelThreads) {
+  for (int e = tid; e < kMaxExperts; e += kSelThreads) {
     sh.votes[e] = 0;
-    sh.anchor[e] = 0;
-    sh.inS[e] = 0;
-    sh.inSp[e] = 0;
-    sh.routed[e] = 0;
-    sh.resident[e] = has_mask ? (p.resident[e] != 0) : 1;
+    sh.rankv[e] = 0;
+    sh.anchor[e] = sh.inR[e] = sh.inS[e] = sh.inC[e] = sh.inSp[e] = sh.routed[e] = 0;
+    sh.u[e] = 0.0;
+    sh.score[e] = 0.0;
+    sh.resident[e] = (e < E) ? (has_mask ? (p.resident[e] != 0) : 1) : 0;
   }
-  __syncthreads();
-  for (int tl = tid; tl < Tb; tl += kSelThreads) {
-    const int t = t_begin + tl;
-    const int d = p.depth[t];
+  if (tid < kRoutedWords) p.ws_routed[b * kRoutedWords + tid] = 0u;
+  int my_d = -1;
+  float my_p = 0.0f;
+  if (tid < Tb) {
+    const int t = t_begin + tid;
+    my_d = p.depth[t];
+    my_p = p.prob[t];
+    const int par = p.parent != nullptr ? p.parent[t] : 0;
+    const int par_d = (p.parent != nullptr && tid > 0 && par >= t_begin && par < t) ? p.depth[par] : 0;
     int code = 0;
-    if (tl == 0) {
-      if (d != 0 || (p.parent != nullptr && p.parent[t] != -1)) code = CODE_ROOT;
+    if (tid == 0) {
+      if (my_d != 0 || (p.parent != nullptr && par != -1)) code = CODE_ROOT;
     } else if (p.parent != nullptr) {
-      const int par = p.parent[t];
       if (par < t_begin || par >= t) code = CODE_PARENT;
-      else if (d != p.depth[par] + 1) code = CODE_DEPTH;
-    } else if (d < 1 || d >= Tb) {
+      else if (my_d != par_d + 1) code = CODE_DEPTH;
+    } else if (my_d < 1 || my_d >= Tb) {
       code = CODE_DEPTH;
     }
-    const float pr = p.prob[t];
-    if (!(pr >= 0.0f) || !isfinite(pr)) code = code ? code : CODE_PROB;
+    if (!(my_p >= 0.0f) || !isfinite(my_p)) code = code ? code : CODE_PROB;
     if (code) atomicMin(&sh.code, code);
-    if (d >= 0 && d < Tb) atomicAdd(&sh.Nd[d], 1);
+    if (my_d >= 0 && my_d < Tb) atomicAdd(&sh.Nd[my_d], 1);
   }
   __syncthreads();
   const int code = (sh.code == 0x7fffffff) ? 0 : sh.code;
 
   if (code != 0) {
-    // invalid tree: no routing for its nodes
-    for (int i = tid; i < Tb * k; i += kSelThreads) {
-      p.topk_idx[static_cast<size_t>(t_begin) * k + i] = -1;
-      p.topk_gate[static_cast<size_t>(t_begin) * k + i] = 0.0f;
-    }
+    // invalid tree: an empty eligible set, so its nodes get no routing
     for (int e = tid; e < E; e += kSelThreads) p.eligible[static_cast<size_t>(b) * E + e] = 0;
     if (p.stats != nullptr && tid < kNumStats) {
       int v = 0;
@@ -179,58 +301,15 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Tre
     }
     return;
   }
-
-  // ---------------- P2: natural top-k, softmax, contributions ----------------
-  uint32_t* sk = sh.sk[wave];
-  int* se = sh.se[wave];
-  float* sz = sh.sz[wave];
-  for (int tl = wave; tl < Tb; tl += kSelWaves) {
-    const int t = t_begin + tl;
-    const float* zrow = p.logits + static_cast<size_t>(t) * E;
-    float zv[EPL];
-    uint32_t key[EPL];
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      const int e = lane + kWave * i;
-      zv[i] = e < E ? zrow[e] : -INFINITY;
-      key[i] = e < E ? logit_key(zv[i]) : 0u;
-    }
-    // softmax over all E in fp64 (max subtracted)
-    float zmax = zv[0];
-#pragma unroll
-    for (int i = 1; i < EPL; ++i) zmax = fmaxf(zmax, zv[i]);
-    zmax = wave_max_f32(zmax);
-    double den = 0.0;
-#pragma unroll
-    for (int i = 0; i < EPL; ++i)
-      if (lane + kWave * i < E) den += exp(static_cast<double>(zv[i]) - static_cast<double>(zmax));
-    den = wave_sum_f64(den);
-    if (p.mode == MODE_MOESPEC) {
-#pragma unroll
-      for (int i = 0; i < EPL; ++i) {
-        const int e = lane + kWave * i;
-        if (e < E)
-          p.ws_rfull[static_cast<size_t>(t) * E + e] =
-              exp(static_cast<double>(zv[i]) - static_cast<double>(zmax)) / den;
-      }
-    }
-    const int d = p.depth[t];
-    const double alpha = pow(static_cast<double>(p.prob[t]), p.beta) / sqrt(static_cast<double>(sh.Nd[d]));
-    const int n = wave_topk_compact<EPL>(key, zv, k, lane, sk, se, sz);
-    if (lane < n) {
-      const int slot = slot_of(lane, n, sk, se);
-      const int e = se[lane];
-      const double r = exp(static_cast<double>(sz[lane]) - static_cast<double>(zmax)) / den;
-      p.ws_kidx[static_cast<size_t>(t) * k + slot] = e;
-      p.ws_contrib[static_cast<size_t>(t) * k + slot] = alpha * r;
-      atomicAdd(&sh.votes[e], 1);
-      if (d == 0) sh.anchor[e] = 1;
-    }
-    wave_lds_sync();
+  // alpha_t = p_t^beta / sqrt(N_{d_t})   (Eq. 3)
+  if (tid < Tb) {
+    const double pd = static_cast<double>(my_p);
+    const double pb = p.beta == 0.5 ? sqrt(pd) : (p.beta == 1.0 ? pd : pow(pd, p.beta));
+    sh.alpha[tid] = pb / sqrt(static_cast<double>(sh.Nd[my_d]));
   }
   __syncthreads();
 
-  // ---------------- P3: utility in node order ----------------
+  // ---------------- P3: votes, anchor, utility in node order ----------------
   double u_acc = 0.0;
   const int chunk = kDenseDoubles / E;  // >= 8 for E <= 512
   for (int c0 = 0; c0 < Tb; c0 += chunk) {
@@ -241,34 +320,39 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Tre
       const int tl = c0 + i / k;
       const size_t gi = static_cast<size_t>(t_begin + tl) * k + (i % k);
       const int e = p.ws_kidx[gi];
-      sh.dense[(tl - c0) * E + e] = p.ws_contrib[gi];
+      sh.dense[(tl - c0) * E + e] = sh.alpha[tl] * p.ws_r[gi];
+      atomicAdd(&sh.votes[e], 1);
+      if (tl == 0) sh.anchor[e] = 1;  // the root is the tree's only depth-0 node
     }
     __syncthreads();
-    if (tid < E)
+    if (tid < E) {
+#pragma unroll 8
       for (int j = 0; j < cn; ++j) u_acc += sh.dense[j * E + tid];
+    }
     __syncthreads();
   }
-  if (tid < E) sh.u[tid] = u_acc;
+  {
+    const bool in_e = tid < E;
+    const bool anc = in_e && sh.anchor[tid];
+    if (in_e) {
+      sh.u[tid] = u_acc;
+      sh.inR[tid] = !anc;
+    }
+    wg_count(anc, &sh.n_anchor, lane);
+    wg_count(in_e && sh.votes[tid] > 0, &sh.n_unat, lane);
+    wg_count(in_e && !anc, &sh.n_R, lane);
+    wg_count(in_e && !anc && u_acc > 0.0, &sh.n_pos, lane);
+  }
   __syncthreads();
 
   // ---------------- P4: eligible set ----------------
-  // counts: |A|, |U_nat|, |R|, #positive residual
-  if (tid < E) {
-    if (sh.anchor[tid]) atomicAdd(&sh.n_anchor, 1);
-    if (sh.votes[tid] > 0) atomicAdd(&sh.n_unat, 1);
-    if (!sh.anchor[tid]) {
-      atomicAdd(&sh.n_R, 1);
-      if (sh.u[tid] > 0.0) atomicAdd(&sh.n_pos, 1);
-    }
-  }
-  __syncthreads();
   const int mode = p.mode;
   const int kmin = min(k, E);
-  int bud = p.budget < kmin ? kmin : (p.budget > E ? E : p.budget);
+  const int bud = p.budget < kmin ? kmin : (p.budget > E ? E : p.budget);
 
   if (mode == MODE_SELF) {
-    // Z = sum over R of u^+ ; H = -sum q log q ; n_er = ceil(exp(H) - 1e-9)
-    if (tid < E) sh.dense[tid] = (!sh.anchor[tid] && sh.u[tid] > 0.0) ? sh.u[tid] : 0.0;
+    // Z = sum over R of u^+ ; H = -sum q log q ; n_er = ceil(exp(H) - 1e-9)   (Eq. 6)
+    if (tid < E) sh.dense[tid] = (sh.inR[tid] && sh.u[tid] > 0.0) ? sh.u[tid] : 0.0;
     __syncthreads();
     const double Z = wg_sum_experts(sh.dense, E, wave, lane);
     if (tid == 0) sh.Z = Z;
@@ -295,7 +379,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Tre
       }
       sh.n_er = ner;
       int take = ner;
-      if (sh.n_anchor + take < kmin) take = kmin - sh.n_anchor;
+      if (sh.n_anchor + take < kmin) take = kmin - sh.n_anchor;  // |S| >= k
       if (take > sh.n_R) take = sh.n_R;
       sh.n_take = take;
     }
@@ -307,91 +391,73 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Tre
       sh.n_er = take;
       sh.n_take = take;
     }
-  }
-  __syncthreads();
-
-  if (mode == MODE_SELF || mode == MODE_FIXED) {
-    // rank within R by (u desc, index asc); S = A u first n_take of R
+  } else if (mode == MODE_MOESPEC || mode == MODE_COUNT) {
+    // MoE-Spec: router mass summed over the block; Count-B: natural votes
     if (tid < E) {
-      bool in = sh.anchor[tid] != 0;
-      if (!in) {
-        const double ue = sh.u[tid];
-        int r = 0;
-        for (int j = 0; j < E; ++j)
-          if (!sh.anchor[j]) {
-            const double uj = sh.u[j];
-            r += (uj > ue) || (uj == ue && j < tid);
-          }
-        in = r < sh.n_take;
-      }
-      sh.inS[tid] = in;
-    }
-  } else if (mode == MODE_ALL) {
-    if (tid < E) sh.inS[tid] = 1;
-  } else {
-    // MoE-Spec (summed router mass) or Count-B (votes): top-bud of all experts
-    double score = 0.0;
-    if (tid < E) {
+      double score = 0.0;
       if (mode == MODE_MOESPEC) {
+#pragma unroll 8
         for (int tl = 0; tl < Tb; ++tl) score += p.ws_rfull[static_cast<size_t>(t_begin + tl) * E + tid];
       } else {
         score = static_cast<double>(sh.votes[tid]);
       }
-      sh.dense[tid] = score;
-    }
-    __syncthreads();
-    if (tid < E) {
-      int r = 0;
-      for (int j = 0; j < E; ++j) {
-        const double sj = sh.dense[j];
-        r += (sj > score) || (sj == score && j < tid);
-      }
-      sh.inS[tid] = r < bud;
+      sh.score[tid] = score;
+      sh.inC[tid] = 1;  // every expert competes
     }
   }
   __syncthreads();
 
-  // |S|, a(S)
-  if (tid < E) {
-    if (sh.inS[tid]) atomicAdd(&sh.n_S, 1);
-    if (!sh.inS[tid] && sh.votes[tid] > 0) atomicAdd(&sh.budget_a, sh.votes[tid]);
+  if (mode == MODE_SELF || mode == MODE_FIXED) {
+    // S = A u first n_take of R in (u desc, index asc) order
+    rank_all<true>(sh.u, sh.inR, E, sh.rankv, tid);
+    __syncthreads();
+    if (tid < E) sh.inS[tid] = sh.anchor[tid] || sh.rankv[tid] < sh.n_take;
+  } else if (mode == MODE_ALL) {
+    if (tid < E) sh.inS[tid] = 1;
+  } else {
+    rank_all<true>(sh.score, sh.inC, E, sh.rankv, tid);
+    __syncthreads();
+    if (tid < E) sh.inS[tid] = sh.rankv[tid] < bud;
   }
   __syncthreads();
-  if (mode == MODE_ALL) {
-    if (tid == 0) {
-      sh.n_er = E - sh.n_anchor;
-      sh.budget_a = 0;
-    }
-  } else if (mode == MODE_MOESPEC || mode == MODE_COUNT) {
-    // members outside the anchor
-    if (tid < E && sh.inS[tid] && !sh.anchor[tid]) atomicAdd(&sh.n_er, 1);
+  if (tid < E) sh.rankv[tid] = 0;
+
+  // |S|, a(S)
+  {
+    const bool in_e = tid < E;
+    const bool inS = in_e && sh.inS[tid];
+    if (in_e) sh.inC[tid] = 0;
+    wg_count(inS, &sh.n_S, lane);
+    wg_add((in_e && !inS) ? sh.votes[tid] : 0, &sh.budget_a, lane);
+    wg_count((mode == MODE_MOESPEC || mode == MODE_COUNT) && inS && !sh.anchor[tid], &sh.n_er, lane);
+  }
+  __syncthreads();
+  if (mode == MODE_ALL && tid == 0) {
+    sh.n_er = E - sh.n_anchor;
+    sh.budget_a = 0;
   }
 
   const bool prune = has_mask && (mode == MODE_SELF || mode == MODE_FIXED);
   if (prune) {
-    // C = nonresident members of S ordered by (u asc, index asc)
-    if (tid < E) {
-      const bool inC = sh.inS[tid] && !sh.resident[tid];
-      sh.rankv[tid] = -1;
-      if (inC) {
-        atomicAdd(&sh.n_C, 1);
-        const double ue = sh.u[tid];
-        int r = 0;
-        for (int j = 0; j < E; ++j)
-          if (sh.inS[j] && !sh.resident[j]) {
-            const double uj = sh.u[j];
-            r += (uj < ue) || (uj == ue && j < tid);
-          }
-        sh.rankv[tid] = r;
-        sh.pv[r] = sh.votes[tid];
-      }
+    // C = nonresident members of S ordered by (u asc, index asc)   (Sec. 3.4)
+    {
+      const bool c = tid < E && sh.inS[tid] && !sh.resident[tid];
+      if (tid < E) sh.inC[tid] = c;
+      wg_count(c, &sh.n_C, lane);
     }
     __syncthreads();
+    rank_all<false>(sh.u, sh.inC, E, sh.rankv, tid);
+    __syncthreads();
+    if (tid < E) {
+      if (sh.inC[tid]) sh.pv[sh.rankv[tid]] = sh.votes[tid];
+      else sh.rankv[tid] = -1;
+    }
+    __syncthreads();
+    // m* = longest prefix with sum v <= a(S), |S| - m >= k, m <= removal cap   (Eq. 7)
     if (tid == 0) {
-      int cap = p.removal_cap < 0 ? E : p.removal_cap;
       int limit = sh.n_C;
       if (sh.n_S - k < limit) limit = sh.n_S - k;
-      if (cap < limit) limit = cap;
+      if (p.removal_cap < limit) limit = p.removal_cap;
       if (limit < 0) limit = 0;
       int m = 0, acc = 0;
       while (m < limit && acc + sh.pv[m] <= sh.budget_a) {
@@ -406,47 +472,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Tre
     if (tid < E) sh.inSp[tid] = sh.inS[tid];
   }
   __syncthreads();
-  if (tid < E && sh.inSp[tid]) atomicAdd(&sh.n_Sp, 1);
 
-  // ---------------- P5: restricted top-k and gates ----------------
-  for (int tl = wave; tl < Tb; tl += kSelWaves) {
-    const int t = t_begin + tl;
-    const float* zrow = p.logits + static_cast<size_t>(t) * E;
-    float zv[EPL];
-    uint32_t key[EPL];
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      const int e = lane + kWave * i;
-      const bool ok = e < E && sh.inSp[e];
-      zv[i] = ok ? zrow[e] : -INFINITY;
-      key[i] = ok ? logit_key(zv[i]) : 0u;
-    }
-    const int n = wave_topk_compact<EPL>(key, zv, k, lane, sk, se, sz);
-    // gates: softmax over the selected logits, fp64
-    double zm = lane < n ? static_cast<double>(sz[lane]) : -INFINITY;
-    zm = wave_max_f64(zm);
-    const double w = lane < n ? exp(static_cast<double>(sz[lane]) - zm) : 0.0;
-    const double ws = wave_sum_f64(w);
-    int32_t* orow = p.topk_idx + static_cast<size_t>(t) * k;
-    float* grow = p.topk_gate + static_cast<size_t>(t) * k;
-    if (lane < n) {
-      const int slot = slot_of(lane, n, sk, se);
-      orow[slot] = se[lane];
-      grow[slot] = static_cast<float>(w / ws);
-      sh.routed[se[lane]] = 1;
-    } else if (lane < k) {
-      orow[lane] = -1;  // fewer eligible experts than k (cannot happen when |S'| >= k)
-      grow[lane] = 0.0f;
-    }
-    wave_lds_sync();
-  }
-  __syncthreads();
-
-  // ---------------- P6: outputs ----------------
-  if (tid < E) {
-    p.eligible[static_cast<size_t>(b) * E + tid] = sh.inSp[tid];
-    if (sh.routed[tid]) atomicAdd(&sh.n_routed, 1);
-  }
+  // ---------------- outputs ----------------
+  if (tid < E) p.eligible[static_cast<size_t>(b) * E + tid] = sh.inSp[tid];
+  wg_count(tid < E && sh.inSp[tid], &sh.n_Sp, lane);
   __syncthreads();
   if (p.stats != nullptr && tid == 0) {
     int32_t* st = p.stats + b * kNumStats;
@@ -459,7 +488,61 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Tre
     st[6] = sh.budget_a;
     st[7] = sh.m_star;
     st[8] = 0;
-    st[9] = sh.n_routed;
+    st[9] = 0;  // routed experts, counted by restricted_kernel
+  }
+}
+
+// ---------------------------------------------------------------------------
+// restricted top-k over S' and renormalised gates, one wave per node
+// ---------------------------------------------------------------------------
+template <int EPL>
+__global__ __launch_bounds__(kNodeWaves * kWave) void restricted_kernel(SelectParams p, TreeOffsets offs) {
+  __shared__ NodeScratch ns;
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int t = blockIdx.x * kNodeWaves + wave;
+  if (t >= p.T) return;
+  const int E = p.E, k = p.k;
+  // tree of node t: the b with o[b] <= t < o[b+1] (empty trees are skipped)
+  int lo = 0, hi = p.B - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (offs.o[mid] <= t) lo = mid;
+    else hi = mid - 1;
+  }
+  const int b = lo;
+  const uint8_t* elig = p.eligible + static_cast<size_t>(b) * E;
+  float zv[EPL];
+  uint32_t key[EPL];
+  load_row<EPL>(p.logits + static_cast<size_t>(t) * E, E, lane, zv);
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + kWave * i;
+    key[i] = (e < E && elig[e]) ? logit_key(zv[i]) : 0u;
+  }
+  uint32_t* sk = ns.sk[wave];
+  int* se = ns.se[wave];
+  float* sz = ns.sz[wave];
+  const int n = wave_topk_compact<EPL>(key, zv, k, lane, sk, se, sz);
+  // gates: softmax over the selected logits, fp64
+  double zm = lane < n ? static_cast<double>(sz[lane]) : -INFINITY;
+  zm = wave_max_f64(zm);
+  const double w = lane < n ? exp(static_cast<double>(sz[lane]) - zm) : 0.0;
+  const double ws = wave_sum_f64(w);
+  int32_t* orow = p.topk_idx + static_cast<size_t>(t) * k;
+  float* grow = p.topk_gate + static_cast<size_t>(t) * k;
+  if (lane < n) {
+    const int slot = slot_of(lane, n, sk, se);
+    const int e = se[lane];
+    orow[slot] = e;
+    grow[slot] = static_cast<float>(w / ws);
+    if (p.stats != nullptr) {
+      const uint32_t bit = 1u << (e & 31);
+      const uint32_t old = atomicOr(&p.ws_routed[b * kRoutedWords + (e >> 5)], bit);
+      if (!(old & bit)) atomicAdd(&p.stats[b * kNumStats + 9], 1);
+    }
+  } else if (lane < k) {
+    orow[lane] = -1;  // fewer eligible experts than k (an invalid tree has none)
+    grow[lane] = 0.0f;
   }
 }
 
@@ -470,7 +553,7 @@ size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 size_t select_workspace_bytes(int T, int E, int k) {
   const size_t Tt = static_cast<size_t>(T > 0 ? T : 0);
   return align256(Tt * k * sizeof(int32_t)) + align256(Tt * k * sizeof(double)) +
-         align256(Tt * E * sizeof(double));
+         align256(Tt * E * sizeof(double)) + align256(sizeof(uint32_t) * kMaxTrees * kRoutedWords);
 }
 
 void select_carve(void* ws, int T, int E, int k, SelectParams& p) {
@@ -478,23 +561,28 @@ void select_carve(void* ws, int T, int E, int k, SelectParams& p) {
   const size_t Tt = static_cast<size_t>(T > 0 ? T : 0);
   p.ws_kidx = reinterpret_cast<int32_t*>(c);
   c += align256(Tt * k * sizeof(int32_t));
-  p.ws_contrib = reinterpret_cast<double*>(c);
+  p.ws_r = reinterpret_cast<double*>(c);
   c += align256(Tt * k * sizeof(double));
   p.ws_rfull = reinterpret_cast<double*>(c);
+  c += align256(Tt * E * sizeof(double));
+  p.ws_routed = reinterpret_cast<uint32_t*>(c);
+}
+
+template <int EPL>
+hipError_t launch_select_epl(const SelectParams& p, const TreeOffsets& offs, hipStream_t stream) {
+  const int node_blocks = (p.T + kNodeWaves - 1) / kNodeWaves;
+  if (node_blocks > 0) natural_kernel<EPL><<<node_blocks, kNodeWaves * kWave, 0, stream>>>(p);
+  tree_kernel<<<p.B, kSelThreads, 0, stream>>>(p, offs);
+  if (node_blocks > 0) restricted_kernel<EPL><<<node_blocks, kNodeWaves * kWave, 0, stream>>>(p, offs);
+  return hipGetLastError();
 }
 
 hipError_t launch_select(const SelectParams& p, const TreeOffsets& offs, hipStream_t stream) {
   const int epl = (p.E + kWave - 1) / kWave;
-  dim3 grid(p.B), block(kSelThreads);
-  if (epl <= 1)
-    select_kernel<1><<<grid, block, 0, stream>>>(p, offs);
-  else if (epl <= 2)
-    select_kernel<2><<<grid, block, 0, stream>>>(p, offs);
-  else if (epl <= 4)
-    select_kernel<4><<<grid, block, 0, stream>>>(p, offs);
-  else
-    select_kernel<8><<<grid, block, 0, stream>>>(p, offs);
-  return hipGetLastError();
+  if (epl <= 1) return launch_select_epl<1>(p, offs, stream);
+  if (epl <= 2) return launch_select_epl<2>(p, offs, stream);
+  if (epl <= 4) return launch_select_epl<4>(p, offs, stream);
+  return launch_select_epl<8>(p, offs, stream);
 }
 
 }  // namespace amoe

@@ -343,3 +343,43 @@ def test_end_to_end(gpu, name, rho):
     torch.cuda.synchronize()
     assert np.array_equal(out2.cpu().numpy().view(np.uint32), y.view(np.uint32))
     assert np.array_equal(sel2["idx"].cpu().numpy(), got_idx)
+
+
+# ---------------------------------------------------------------------------
+# HIP graph capture of a whole step: every replay equals the eager result
+# ---------------------------------------------------------------------------
+def test_graph_replay_matches_eager(gpu):
+    cfg = W.CONFIGS["qwen3_30b_a3b"]
+    rw = W.router_weights(cfg)
+    wg, wu, wd = W.expert_weights_torch(cfg, 0, DEV)
+    layer = ops.VerifyLayer(f32(rw), wg, wu, wd, cfg.k, max_tokens=cfg.T)
+    blocks = []
+    for b in range(2):
+        blk = W.make_block(cfg, block=b)
+        hdev, _ = hidden_for(cfg, blk.hidden)
+        blocks.append((to_dev_hidden(cfg, hdev), i32(blk.parent), i32(blk.depth), f32(blk.prob)))
+
+    def snap():
+        return (layer.out[:cfg.T].clone(), layer.sel_out["idx"][:cfg.T].clone(),
+                layer.sel_out["eligible"][:1].clone())
+
+    layer.step(*blocks[0])
+    torch.cuda.synchronize()
+    ref = snap()
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            layer.step(*blocks[0])
+    torch.cuda.synchronize()
+    say("graph replay vs eager")
+    for rep in range(3):
+        layer.step(*blocks[1])          # eager work on other inputs in between
+        torch.cuda.synchronize()
+        other = snap()
+        assert not torch.equal(other[0], ref[0])
+        g.replay()
+        torch.cuda.synchronize()
+        got = snap()
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), f"replay {rep} differs"
