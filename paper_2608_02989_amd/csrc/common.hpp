@@ -41,6 +41,14 @@ __device__ __forceinline__ uint32_t logit_key(float z) {
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return static_cast<int>(threadIdx.x & (kWave - 1)); }
 
+// Wave index inside the workgroup as a scalar (SGPR) value.  Without this the
+// compiler treats threadIdx.x / 64 as a per-lane value, turns loops bounded by
+// it into exec-masked branches and places conservative vmcnt waits at their
+// joins (which stalls on prefetched loads).
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
+}
+
 __device__ __forceinline__ uint64_t lanes_below(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }

@@ -184,11 +184,61 @@ struct F32Path {
 
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
+// Tunables (compile-time): k-steps per pipeline stage for small / large
+// M-tile counts; per projection, the output tiles each wave computes on shared
+// A fragments (NTW) and the number of waves splitting a tile's K range (KS).
+#ifndef AMOE_KU_SMALL
+#define AMOE_KU_SMALL 2
+#endif
+#ifndef AMOE_KU_LARGE
+#define AMOE_KU_LARGE 2
+#endif
+#ifndef AMOE_GU_NTW
+#define AMOE_GU_NTW 2
+#endif
+#ifndef AMOE_GU_KS
+#define AMOE_GU_KS 4
+#endif
+#ifndef AMOE_DN_NTW
+#define AMOE_DN_NTW 2
+#endif
+#ifndef AMOE_DN_KS
+#define AMOE_DN_KS 4
+#endif
+
+#ifndef AMOE_NT_WEIGHTS
+#define AMOE_NT_WEIGHTS 1
+#endif
+
+// Weight fragments are read once per step: non-temporal loads keep them from
+// displacing the reused activations in the caches.
+__device__ __forceinline__ uint4 load_weight(const uint4* p) {
+#if AMOE_NT_WEIGHTS
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+#else
+  return *p;
+#endif
+}
+
 // k-steps per pipeline stage; two stages are kept in flight
 template <int MT>
 struct Stage {
-  static constexpr int kU = MT <= 2 ? 4 : 2;
+  static constexpr int kU = MT <= 2 ? AMOE_KU_SMALL : AMOE_KU_LARGE;
 };
+
+// 16-byte LDS pieces per lane for the shared A stages of any pass with up to
+// MTMAX M-tiles (two stages of kU * MT fragments)
+template <int MTMAX>
+constexpr int shared_a_pieces() {
+  int best = 0;
+  for (int mt = 1; mt <= MTMAX; ++mt) {
+    const int ku = mt <= 2 ? AMOE_KU_SMALL : AMOE_KU_LARGE;
+    best = ku * mt > best ? ku * mt : best;
+  }
+  return 2 * best;
+}
 
 // acc[nb][mt] += sum over fragments kc in [kc0, kc1) of x[mt] (A, tokens) times
 // w[nb] (B, weight rows).  w[nb] / x[mt] point at this lane's 16-byte piece of
@@ -204,7 +254,7 @@ __device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const 
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) wb0[u][nb] = w[nb][static_cast<size_t>(c + u) * kWave];
+      for (int nb = 0; nb < NB; ++nb) wb0[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * kWave);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) xb0[u][mt] = x[mt][(c + u) * 4];
     }
@@ -213,7 +263,7 @@ __device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const 
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) wb1[u][nb] = w[nb][static_cast<size_t>(c + u) * kWave];
+      for (int nb = 0; nb < NB; ++nb) wb1[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * kWave);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) xb1[u][mt] = x[mt][(c + u) * 4];
     }
@@ -234,21 +284,130 @@ __device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const 
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = P::mma(xb1[u][mt], wb1[u][nb], acc[nb][mt]);
   };
-  const int full_end = kc0 + (kc1 - kc0) / kU * kU;
-  if (kc0 < full_end) load0(kc0);
-  for (int c = kc0; c < full_end; c += 2 * kU) {
-    const bool has1 = c + kU < full_end;
-    if (has1) load1(c + kU);
-    comp0();
-    if (has1) {
-      if (c + 2 * kU < full_end) load0(c + 2 * kU);
+  // Steady state without branches: the prefetch of the next stage is issued
+  // unconditionally before the current stage is consumed, so the wait-count
+  // pass sees straight-line code and only waits for the stage being used.
+  // The last one or two stages are peeled off after the loop.
+  const int nst = (kc1 - kc0) / kU;
+  const int full_end = kc0 + nst * kU;
+  if (nst > 0) {
+    load0(kc0);
+    int st = 0;
+    for (; st + 2 < nst; st += 2) {
+      load1(kc0 + (st + 1) * kU);
+      comp0();
+      load0(kc0 + (st + 2) * kU);
       comp1();
+    }
+    if (st + 1 < nst) {
+      load1(kc0 + (st + 1) * kU);
+      comp0();
+      comp1();
+    } else {
+      comp0();
     }
   }
   for (int c = full_end; c < kc1; ++c) {
     uint4 wt[NB], xt[MT];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) wt[nb] = w[nb][static_cast<size_t>(c) * kWave];
+    for (int nb = 0; nb < NB; ++nb) wt[nb] = load_weight(w[nb] + static_cast<size_t>(c) * kWave);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) xt[mt] = x[mt][c * 4];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = P::mma(xt[mt], wt[nb], acc[nb][mt]);
+  }
+}
+
+// acc[nb][mt] as in stream_tiles, for a workgroup whose 4 waves all cover the
+// same K range: each A fragment of a stage is loaded from global memory once,
+// by one of the 4 waves, into a double-buffered LDS stage and read from there
+// by all of them.  Weight fragments stay per wave, two stages in flight.  All
+// 4 waves must call this with the same kc range (it contains barriers).
+template <class P, int MT, int NB>
+__device__ __forceinline__ void stream_tiles_shared(const uint4* const (&w)[NB], const uint4* const (&x)[MT],
+                                                    int KC, floatx4 (&acc)[NB][MT], uint4* xs) {
+  constexpr int kU = Stage<MT>::kU;
+  constexpr int kFr = kU * MT;                   // A fragments per stage
+  constexpr int kMine = (kFr + 3) / 4;           // of which this wave loads
+  const int wave = wave_id(), lane = lane_id();
+  // xs layout: [2 stages][kU][MT][64 lanes] 16-byte pieces
+  auto xs_at = [&](int buf, int u, int mt) { return xs + ((buf * kU + u) * MT + mt) * kWave + lane; };
+  uint4 wb0[kU][NB], wb1[kU][NB], ta[kMine];
+  auto loadw0 = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) wb0[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * kWave);
+  };
+  auto loadw1 = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) wb1[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * kWave);
+  };
+  // fragment f of a stage (step f / MT, M-tile f % MT) is loaded by wave f % 4;
+  // every index below is a compile-time constant, the wave test is uniform
+  auto loada = [&](int c) {
+#pragma unroll
+    for (int f = 0; f < kFr; ++f)
+      if ((f & 3) == wave) ta[f >> 2] = x[f % MT][(c + f / MT) * 4];
+  };
+  auto storea = [&](int buf) {
+#pragma unroll
+    for (int f = 0; f < kFr; ++f)
+      if ((f & 3) == wave) *xs_at(buf, f / MT, f % MT) = ta[f >> 2];
+  };
+  auto comp = [&](int buf, uint4 (&wb)[kU][NB]) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      uint4 xa[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) xa[mt] = *xs_at(buf, u, mt);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = P::mma(xa[mt], wb[u][nb], acc[nb][mt]);
+    }
+  };
+  const int nst = KC / kU;  // full stages; a ragged tail follows
+  if (nst > 0) {
+    // stage st lives in LDS buffer st & 1 and registers wb0 / wb1; the
+    // steady state is branch-free, the last one or two stages are peeled
+    loadw0(0);
+    loada(0);
+    storea(0);
+    __syncthreads();
+    int st = 0;
+    for (; st + 2 < nst; st += 2) {
+      loadw1((st + 1) * kU);
+      loada((st + 1) * kU);
+      comp(0, wb0);
+      storea(1);
+      __syncthreads();
+      loadw0((st + 2) * kU);
+      loada((st + 2) * kU);
+      comp(1, wb1);
+      storea(0);
+      __syncthreads();
+    }
+    if (st + 1 < nst) {
+      loadw1((st + 1) * kU);
+      loada((st + 1) * kU);
+      comp(0, wb0);
+      storea(1);
+      __syncthreads();
+      comp(1, wb1);
+    } else {
+      comp(0, wb0);
+    }
+    __syncthreads();  // the LDS stages may be reused by the next pass
+  }
+  for (int c = nst * kU; c < KC; ++c) {
+    uint4 wt[NB], xt[MT];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) wt[nb] = load_weight(w[nb] + static_cast<size_t>(c) * kWave);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) xt[mt] = x[mt][c * 4];
 #pragma unroll
@@ -259,147 +418,150 @@ __device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const 
 }
 
 // ---------------------------------------------------------------------------
-// gate/up + SwiGLU.  One workgroup (4 waves) per (active expert, 16-row tile of
-// I); the waves split the H reduction into 4 contiguous quarters and combine
-// their partial tiles in LDS in a fixed order.  grid.x = cap_experts * (I/16).
+// The two grouped projections share one pass structure.  A workgroup (4
+// waves) owns a run of 16-row output tiles of one active expert.  Each wave
+// computes NTW tiles that share its A fragments; the KS waves of a tile group
+// split the K range and add their partial tiles in LDS in a fixed order
+// (deterministic), so one workgroup covers 4 * NTW / KS tiles.
+//   GateUp: rows of I, K = H, A = gathered hidden rows; each tile has a gate
+//           and an up fragment; SwiGLU -> act (bf16 for the bf16 path, fp32
+//           otherwise), written once per token row.
+//   Down:   rows of H, K = I, A = act rows of the expert; gate-scaled rows go
+//           to the token's slot row of ys.
 // ---------------------------------------------------------------------------
-constexpr int kGuWaves = 4;
+enum class Proj { GateUp, Down };
 
-template <class P, int MT>
-__device__ __forceinline__ void gateup_pass(const ForwardParams& p, int e, int nt, int n_e, int o_e, int m0,
-                                            floatx4 (*red)[kWave][2][4]) {
-  const int wave = threadIdx.x / kWave, lane = lane_id();
+template <Proj F, int NTW, int KS>
+struct ProjShape {
+  static constexpr int kNB = NTW * (F == Proj::GateUp ? 2 : 1);  // weight fragments per k-step
+  static constexpr int kTilesPerWG = 4 * NTW / KS;
+};
+
+template <class P, Proj F, int MT, int NTW, int KS>
+__device__ __forceinline__ void ffn_pass(const ForwardParams& p, int e, int tile_base, int n_e, int o_e, int m0,
+                                         floatx4 (*red)[kWave][4], uint4* xs) {
+  constexpr int NB = ProjShape<F, NTW, KS>::kNB;
+  const int wave = wave_id(), lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
-  const int H = p.H, I = p.I;
-  const int KC = H / P::kKF;
-  const int rowq = H * P::kElemBytes / 16;
-  const int NT = I / 16;
-  const uint4* hid = static_cast<const uint4*>(p.hidden);
-  const int tok0 = p.ent_slot[o_e] / p.k;  // rows past n_e read a valid row; their outputs are dropped
+  const int sub = wave % KS;
+  const int tile0 = tile_base + (wave / KS) * NTW;  // first of this wave's NTW tiles
+  const int ntiles = (F == Proj::GateUp ? p.I : p.H) / 16;
+  const int K = F == Proj::GateUp ? p.H : p.I;
+  const int KC = K / P::kKF;
+  const int rowq = K * P::kElemBytes / 16;
+
   const uint4* x[MT];
+  if (F == Proj::GateUp) {
+    const uint4* hid = static_cast<const uint4*>(p.hidden);
+    const int tok0 = p.ent_slot[o_e] / p.k;  // rows past n_e read a valid row; their outputs are dropped
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = m0 + mt * 16 + r;
-    const int tok = m < n_e ? p.ent_slot[o_e + m] / p.k : tok0;
-    x[mt] = hid + static_cast<size_t>(tok) * rowq + g;
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = m0 + mt * 16 + r;
+      const int tok = m < n_e ? p.ent_slot[o_e + m] / p.k : tok0;
+      x[mt] = hid + static_cast<size_t>(tok) * rowq + g;
+    }
+  } else {
+    const uint4* act = static_cast<const uint4*>(p.act);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = m0 + mt * 16 + r;
+      x[mt] = act + static_cast<size_t>(o_e + (m < n_e ? m : 0)) * rowq + g;
+    }
   }
-  const size_t frag0 = (static_cast<size_t>(e) * NT + nt) * KC;
-  const uint4* w[2] = {static_cast<const uint4*>(p.w_gate) + frag0 * kWave + lane,
-                       static_cast<const uint4*>(p.w_up) + frag0 * kWave + lane};
-  floatx4 acc[2][MT];
+  // tiles past the end are clamped to a valid tile: computed, never written
+  const uint4* w[NB];
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb)
+  for (int j = 0; j < NTW; ++j) {
+    const int tile = min(tile0 + j, ntiles - 1);
+    const size_t frag0 = (static_cast<size_t>(e) * ntiles + tile) * KC;
+    if (F == Proj::GateUp) {
+      w[2 * j] = static_cast<const uint4*>(p.w_gate) + frag0 * kWave + lane;
+      w[2 * j + 1] = static_cast<const uint4*>(p.w_up) + frag0 * kWave + lane;
+    } else {
+      w[j] = static_cast<const uint4*>(p.w_down) + frag0 * kWave + lane;
+    }
+  }
+  floatx4 acc[NB][MT];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int kc0 = wave * KC / kGuWaves, kc1 = (wave + 1) * KC / kGuWaves;
-  stream_tiles<P, MT, 2>(w, x, kc0, kc1, acc);
+  if constexpr (KS == 1)
+    stream_tiles_shared<P, MT, NB>(w, x, KC, acc, xs);
+  else
+    stream_tiles<P, MT, NB>(w, x, sub * KC / KS, (sub + 1) * KC / KS, acc);
+
+  if constexpr (KS > 1) {
+    // fixed-order sum of the KS partial tiles, four fragments per LDS round
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    red[wave][lane][0][mt] = acc[0][mt];
-    red[wave][lane][1][mt] = acc[1][mt];
-  }
-  __syncthreads();
-  // wave w finishes M-tiles w, w+4, ...: fixed-order sum over the 4 K quarters
-  for (int mt = wave; mt < MT; mt += kGuWaves) {
-    floatx4 sg = red[0][lane][0][mt], su = red[0][lane][1][mt];
+    for (int q0 = 0; q0 < NB * MT; q0 += 4) {
 #pragma unroll
-    for (int w2 = 1; w2 < kGuWaves; ++w2) {
-      const floatx4 qg = red[w2][lane][0][mt], qu = red[w2][lane][1][mt];
+      for (int q = 0; q < 4; ++q)
+        if (q0 + q < NB * MT) red[wave][lane][q] = acc[(q0 + q) / MT][(q0 + q) % MT];
+      __syncthreads();
+      if (sub == 0) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sg[i] += qg[i];
-        su[i] += qu[i];
+        for (int s2 = 1; s2 < KS; ++s2)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (q0 + q < NB * MT) {
+              const floatx4 v = red[wave + s2][lane][q];
+#pragma unroll
+              for (int i = 0; i < 4; ++i) acc[(q0 + q) / MT][(q0 + q) % MT][i] += v[i];
+            }
       }
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + mt * 16 + 4 * g + i;
-      if (m < n_e) {
-        const float v = silu_mul(sg[i], su[i]);
-        const size_t idx = static_cast<size_t>(o_e + m) * I + nt * 16 + r;
-        if (P::kElemBytes == 2)
-          static_cast<uint16_t*>(p.act)[idx] = float_to_bf16_bits(v);
-        else
-          static_cast<float*>(p.act)[idx] = v;
-      }
+      __syncthreads();
     }
   }
-  __syncthreads();
+  if (sub == 0) {
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      const int tile = tile0 + j;
+      if (tile >= ntiles) continue;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = m0 + mt * 16 + 4 * g + i;
+          if (m < n_e) {
+            if (F == Proj::GateUp) {
+              const float v = silu_mul(acc[2 * j][mt][i], acc[2 * j + 1][mt][i]);
+              const size_t idx = static_cast<size_t>(o_e + m) * p.I + tile * 16 + r;
+              if (P::kElemBytes == 2)
+                static_cast<uint16_t*>(p.act)[idx] = float_to_bf16_bits(v);
+              else
+                static_cast<float*>(p.act)[idx] = v;
+            } else {
+              const int s = p.ent_slot[o_e + m];
+              p.ys[static_cast<size_t>(s) * p.H + tile * 16 + r] = p.topk_gate[s] * acc[j][mt][i];
+            }
+          }
+        }
+      }
+    }
+  }
 }
 
-template <class P, int MTMAX>
-__global__ __launch_bounds__(256) void gateup_kernel(ForwardParams p) {
-  __shared__ floatx4 red[kGuWaves][kWave][2][4];
-  const int NT = p.I / 16;
-  const int a = blockIdx.x / NT;
-  const int nt = blockIdx.x % NT;
+// grid.x = cap_experts * ceil(ntiles / tiles_per_wg)
+template <class P, Proj F, int MTMAX, int NTW, int KS>
+__global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
+  __shared__ floatx4 red[KS > 1 ? 4 : 1][kWave][4];
+  __shared__ uint4 xs[KS == 1 ? shared_a_pieces<MTMAX>() * kWave : 1];
+  constexpr int tpw = ProjShape<F, NTW, KS>::kTilesPerWG;
+  const int ntiles = (F == Proj::GateUp ? p.I : p.H) / 16;
+  const int wg_per_expert = (ntiles + tpw - 1) / tpw;
+  const int a = blockIdx.x / wg_per_expert;
+  const int tile_base = (blockIdx.x % wg_per_expert) * tpw;
   if (a >= *p.n_active) return;
   const int e = p.active[a];
   const int n_e = p.cnt[e];
   const int o_e = p.off[e];
   for (int m0 = 0; m0 < n_e; m0 += 16 * MTMAX) {
     const int nmt = min(MTMAX, (n_e - m0 + 15) / 16);
-    if (nmt == 1) gateup_pass<P, 1>(p, e, nt, n_e, o_e, m0, red);
-    else if (MTMAX >= 2 && nmt == 2) gateup_pass<P, (MTMAX >= 2 ? 2 : 1)>(p, e, nt, n_e, o_e, m0, red);
-    else if (MTMAX >= 3 && nmt == 3) gateup_pass<P, (MTMAX >= 3 ? 3 : 1)>(p, e, nt, n_e, o_e, m0, red);
-    else gateup_pass<P, MTMAX>(p, e, nt, n_e, o_e, m0, red);
-  }
-}
-
-// ---------------------------------------------------------------------------
-// down projection.  Wave w of workgroup (a, q) owns H-tile ht = 4q + w of
-// active expert a over the whole I reduction.  grid.x = cap_experts * ceil(HT/4).
-// ---------------------------------------------------------------------------
-template <class P, int MT>
-__device__ __forceinline__ void down_pass(const ForwardParams& p, int e, int ht, int n_e, int o_e, int m0) {
-  const int lane = lane_id();
-  const int r = lane & 15, g = lane >> 4;
-  const int H = p.H, I = p.I;
-  const int KC = I / P::kKF;
-  const int rowq = I * P::kElemBytes / 16;
-  const int HT = H / 16;
-  const uint4* act = static_cast<const uint4*>(p.act);
-  const uint4* x[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = m0 + mt * 16 + r;
-    x[mt] = act + static_cast<size_t>(o_e + (m < n_e ? m : 0)) * rowq + g;
-  }
-  const size_t frag0 = (static_cast<size_t>(e) * HT + ht) * KC;
-  const uint4* w[1] = {static_cast<const uint4*>(p.w_down) + frag0 * kWave + lane};
-  floatx4 acc[1][MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) acc[0][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  stream_tiles<P, MT, 1>(w, x, 0, KC, acc);
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + mt * 16 + 4 * g + i;
-      if (m < n_e) {
-        const int s = p.ent_slot[o_e + m];
-        p.ys[static_cast<size_t>(s) * H + ht * 16 + r] = p.topk_gate[s] * acc[0][mt][i];
-      }
-    }
-  }
-}
-
-template <class P, int MTMAX>
-__global__ __launch_bounds__(256) void down_kernel(ForwardParams p) {
-  const int HT = p.H / 16;
-  const int wg_per_expert = (HT + 3) / 4;
-  const int a = blockIdx.x / wg_per_expert;
-  const int ht = (blockIdx.x % wg_per_expert) * 4 + threadIdx.x / kWave;
-  if (a >= *p.n_active || ht >= HT) return;
-  const int e = p.active[a];
-  const int n_e = p.cnt[e];
-  const int o_e = p.off[e];
-  for (int m0 = 0; m0 < n_e; m0 += 16 * MTMAX) {
-    const int nmt = min(MTMAX, (n_e - m0 + 15) / 16);
-    if (nmt == 1) down_pass<P, 1>(p, e, ht, n_e, o_e, m0);
-    else if (MTMAX >= 2 && nmt == 2) down_pass<P, (MTMAX >= 2 ? 2 : 1)>(p, e, ht, n_e, o_e, m0);
-    else if (MTMAX >= 3 && nmt == 3) down_pass<P, (MTMAX >= 3 ? 3 : 1)>(p, e, ht, n_e, o_e, m0);
-    else down_pass<P, MTMAX>(p, e, ht, n_e, o_e, m0);
+    if (nmt == 1) ffn_pass<P, F, 1, NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
+    else if (MTMAX >= 2 && nmt == 2) ffn_pass<P, F, (MTMAX >= 2 ? 2 : 1), NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
+    else if (MTMAX >= 3 && nmt == 3) ffn_pass<P, F, (MTMAX >= 3 ? 3 : 1), NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
+    else ffn_pass<P, F, MTMAX, NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
   }
 }
 
@@ -437,12 +599,14 @@ __global__ __launch_bounds__(256) void combine_kernel(ForwardParams p) {
 
 template <class P, int MTMAX>
 hipError_t launch_ffn(const ForwardParams& p, int cap, hipStream_t stream) {
-  const int gu_wg = p.I / 16;
-  const int dn_wg = (p.H / 16 + 3) / 4;
-  gateup_kernel<P, MTMAX><<<dim3(cap * gu_wg), 256, 0, stream>>>(p);
+  constexpr int gt = ProjShape<Proj::GateUp, AMOE_GU_NTW, AMOE_GU_KS>::kTilesPerWG;
+  constexpr int dt = ProjShape<Proj::Down, AMOE_DN_NTW, AMOE_DN_KS>::kTilesPerWG;
+  const int gu_wg = (p.I / 16 + gt - 1) / gt;
+  const int dn_wg = (p.H / 16 + dt - 1) / dt;
+  ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS><<<dim3(cap * gu_wg), 256, 0, stream>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  down_kernel<P, MTMAX><<<dim3(cap * dn_wg), 256, 0, stream>>>(p);
+  ffn_kernel<P, Proj::Down, MTMAX, AMOE_DN_NTW, AMOE_DN_KS><<<dim3(cap * dn_wg), 256, 0, stream>>>(p);
   return hipGetLastError();
 }
 

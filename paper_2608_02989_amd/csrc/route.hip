@@ -28,7 +28,7 @@ __global__ __launch_bounds__(kRouteWaves * kWave) void route_kernel(const TIn* _
                                                                    const float* __restrict__ w, int T, int H,
                                                                    int E, float* __restrict__ logits) {
   __shared__ floatx4 part[kRouteWaves][kWave];
-  const int wave = threadIdx.x / kWave;
+  const int wave = wave_id();
   const int lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
   const int e0 = blockIdx.x * 16, t0 = blockIdx.y * 16;

@@ -196,7 +196,7 @@ __device__ __forceinline__ void load_row(const float* __restrict__ zrow, int E, 
 template <int EPL>
 __global__ __launch_bounds__(kNodeWaves * kWave) void natural_kernel(SelectParams p) {
   __shared__ NodeScratch ns;
-  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int wave = wave_id(), lane = lane_id();
   const int t = blockIdx.x * kNodeWaves + wave;
   if (t >= p.T) return;
   const int E = p.E, k = p.k;
@@ -243,7 +243,7 @@ __global__ __launch_bounds__(kNodeWaves * kWave) void natural_kernel(SelectParam
 __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeOffsets offs) {
   __shared__ SelShared sh;
   const int tid = threadIdx.x;
-  const int wave = tid / kWave, lane = lane_id();
+  const int wave = wave_id(), lane = lane_id();
   const int b = blockIdx.x;
   const int t_begin = offs.o[b];
   const int Tb = offs.o[b + 1] - t_begin;
@@ -498,7 +498,7 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
 template <int EPL>
 __global__ __launch_bounds__(kNodeWaves * kWave) void restricted_kernel(SelectParams p, TreeOffsets offs) {
   __shared__ NodeScratch ns;
-  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int wave = wave_id(), lane = lane_id();
   const int t = blockIdx.x * kNodeWaves + wave;
   if (t >= p.T) return;
   const int E = p.E, k = p.k;
