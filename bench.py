@@ -42,11 +42,59 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
     ap.add_argument("--no-alt", action="store_true", help="skip the i.i.d. (rho = 0) companion run")
     ap.add_argument("--graph", type=int, default=1, help="time HIP-graph replays of the step sequence (1/0)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
+                    help="only run a plain device copy of MB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "moe_forward_qwen3_30b_a3b_traffic.md")
+FFN_SOURCES = ["paper_2608_02989_amd/csrc/forward.hip", "paper_2608_02989_amd/csrc/common.hpp"]
+
+
+def ffn_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in FFN_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """Measured / algorithmic HBM bytes of a forward launch from the committed
+    counter summary, or None when it is missing or the kernels changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    vals = {}
+    for line in text.splitlines():
+        if line.startswith("traffic:"):
+            for kv in line[len("traffic:"):].split():
+                k, _, v = kv.partition("=")
+                vals[k] = v
+    if vals.get("source_hash") != ffn_source_hash() or "ratio" not in vals:
+        return None
+    return float(vals["ratio"])
+
+
+def copy_calibration(mb: int) -> None:
+    import torch
+    n = mb << 20
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(f"copied {mb} MiB five times", flush=True)
 
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this layer runs on a single MI355X "
               "(multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
@@ -237,7 +285,9 @@ def main():
                    "natural_union": round(main_m["unat"], 2)},
         "roofline": {"bound": "hbm", "kernel": "acceptmoe_moe_forward (dispatch+gate_up+down+combine)",
                      "achieved": round(main_m["fwd_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(frac, 4), "traffic": None,
+                     "frac": round(frac, 4),
+                     "traffic": (None if measured_traffic() is None
+                                 else round(measured_traffic() * main_m["fwd_bytes_per_launch"])),
                      "bytes_per_launch": round(main_m["fwd_bytes_per_launch"]),
                      "launch_us": round(main_m["fwd_us"], 2),
                      "mfma_util": round(main_m["flops"] / (main_m["fwd_us"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5)},

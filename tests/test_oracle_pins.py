@@ -494,3 +494,24 @@ def test_planted_mistakes_are_caught(monkeypatch):
     monkeypatch.setattr(O, "anchor", lambda K, depth: set(int(e) for e in K[-1]))
     assert _fails(test_hand_example_demand_and_set)
     monkeypatch.setattr(O, "anchor", orig_anchor)
+
+
+# ---------------------------------------------------------------------------
+# router product (Sec. 3.1): brute-force sums and a one-hot special case
+# ---------------------------------------------------------------------------
+def test_route_bruteforce_and_one_hot():
+    rng = np.random.default_rng(21)
+    h = rng.standard_normal((5, 7))
+    w = rng.standard_normal((4, 7))
+    z = O.route(h, w)
+    for t in range(5):
+        for e in range(4):
+            s = 0.0
+            for i in range(7):
+                s += h[t, i] * w[e, i]
+            assert abs(z[t, e] - s) < 1e-12
+    # router row e = unit vector on feature perm[e]: logits pick hidden components
+    perm = np.array([3, 0, 6, 2])
+    onehot = np.zeros((4, 7))
+    onehot[np.arange(4), perm] = 1.0
+    np.testing.assert_array_equal(O.route(h, onehot), h[:, perm])
