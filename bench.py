@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
     ap.add_argument("--no-alt", action="store_true", help="skip the i.i.d. (rho = 0) companion run")
     ap.add_argument("--graph", type=int, default=1, help="time HIP-graph replays of the step sequence (1/0)")
+    ap.add_argument("--stack-blocks", type=int, default=8, help="blocks timed through a whole layer stack")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="only run a plain device copy of MB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -107,6 +108,9 @@ def main():
 
     dev = "cuda"
     cfg = W.CONFIGS[args.config]
+    if cfg.layers > 1:
+        stack_report(args, cfg)
+        return
     Ttot = cfg.total_tokens
     ebytes = cfg.expert_bytes
     layer_bytes = cfg.E * ebytes
@@ -298,6 +302,108 @@ def main():
         "eager_latency_us": round(main_m["eager_us"], 2),
     }
     print(json.dumps(line), flush=True)
+
+
+def _dist(x):
+    x = np.asarray(x, np.float64)
+    return {"mean": round(float(x.mean()), 3), "p10": float(np.percentile(x, 10)),
+            "p50": float(np.percentile(x, 50)), "p90": float(np.percentile(x, 90)),
+            "min": float(x.min()), "max": float(x.max())}
+
+
+def stack_report(args, cfg):
+    """Eligible-set sizes of a 48-layer stack over many seeded blocks, and the
+    latency of a full verify pass through all layers.
+
+    Every (block, layer) pair gets the block's tree (shared by all layers) and
+    its own hidden states and router; route + select run on the GPU and the
+    per-tree statistics are collected on the device.  Then `--stack-blocks`
+    blocks are pushed through all layers (route, select, forward each) with
+    every layer's experts resident.
+    """
+    import torch
+
+    from paper_2608_02989_amd import _lib as L
+    from paper_2608_02989_amd import ops
+    from paper_2608_02989_amd import workload as W
+
+    t0 = time.time()
+
+    def log(msg):
+        print(f"[stack {time.time() - t0:6.1f}s] {msg}", file=sys.stderr, flush=True)
+
+    dev = "cuda"
+    nblocks = args.blocks if args.blocks != 16 else cfg.blocks
+    nl = cfg.layers
+    T, E, k = cfg.T, cfg.E, cfg.k
+    routers = [torch.from_numpy(W.router_weights(cfg, l)).to(dev) for l in range(nl)]
+    logits = torch.empty((T, E), dtype=torch.float32, device=dev)
+    ws = ops.select_workspace(T, E, k, dev)
+    stats_all = torch.empty((nblocks, nl, L.NUM_STATS), dtype=torch.int32, device=dev)
+    outs = {"eligible": torch.empty((1, E), dtype=torch.uint8, device=dev),
+            "idx": torch.empty((T, k), dtype=torch.int32, device=dev),
+            "gate": torch.empty((T, k), dtype=torch.float32, device=dev)}
+    for b in range(nblocks):
+        for l in range(nl):
+            blk = W.make_block(cfg, block=b, layer=l, rho=args.rho, tree_layer=0)
+            h = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(dev)
+            par, dep, prob = (torch.from_numpy(a).to(dev) for a in (blk.parent, blk.depth, blk.prob))
+            ops.route(h, routers[l], out=logits)
+            outs["stats"] = stats_all[b, l:l + 1]
+            ops.select(logits, par, dep, prob, None, k, workspace=ws, outputs=outs)
+        if b % 32 == 31:
+            log(f"{b + 1} blocks selected")
+    torch.cuda.synchronize()
+    st = stats_all.cpu().numpy().reshape(-1, L.NUM_STATS).astype(np.float64)
+    assert (st[:, 8] == 0).all(), "malformed synthetic tree"
+    sp, un, routed, ner = st[:, 4], st[:, 5], st[:, 9], st[:, 2]
+    report = {"report": "eligible-set size distribution", "config": cfg.name, "blocks": nblocks,
+              "layers": nl, "samples": int(st.shape[0]), "T": T, "H": cfg.H, "E": E, "k": k,
+              "rho": args.rho, "eligible_S_prime": _dist(sp), "natural_union": _dist(un),
+              "ratio_S_prime_over_U_nat": _dist(sp / un), "routed_experts": _dist(routed),
+              "n_er": _dist(ner)}
+    log(f"|S'| mean {sp.mean():.2f}, |U_nat| mean {un.mean():.2f}")
+
+    # full 48-layer verify pass for a few blocks, all layers' experts resident
+    layers = []
+    for l in range(nl):
+        wg, wu, wd = W.expert_weights_torch(cfg, l, dev)
+        layers.append(ops.VerifyLayer(routers[l], wg, wu, wd, k, max_tokens=T))
+        del wg, wu, wd
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    log("48 layers packed")
+    nb = args.stack_blocks
+    inputs = []
+    for b in range(nb):
+        per = []
+        for l in range(nl):
+            blk = W.make_block(cfg, block=b, layer=l, rho=args.rho, tree_layer=0)
+            h = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(dev)
+            per.append((h,) + tuple(torch.from_numpy(a).to(dev) for a in (blk.parent, blk.depth, blk.prob)))
+        inputs.append(per)
+    for l in range(nl):
+        layers[l].step(*inputs[0][l])
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for b in range(nb):
+        for l in range(nl):
+            layers[l].step(*inputs[b][l])
+    stop.record()
+    torch.cuda.synchronize()
+    total_us = start.elapsed_time(stop) * 1e3
+    byts = 0.0
+    for b in range(nb):
+        for l in range(nl):
+            layers[l].step(*inputs[b][l])
+            idx = layers[l].sel_out["idx"][:T]
+            byts += int(torch.unique(idx[idx >= 0]).numel()) * cfg.expert_bytes
+    report.update({"stack_pass_blocks": nb, "stack_pass_us_per_block": round(total_us / nb, 1),
+                   "stack_pass_us_per_layer": round(total_us / nb / nl, 2),
+                   "stack_pass_weight_GBs": round(byts / (total_us * 1e-6) / 1e9, 1),
+                   "timing": "eager launches, 48 distinct resident layers per block"})
+    print(json.dumps(report), flush=True)
 
 
 def cpu_baseline(cfg, layers, blocks, budget_s, ebytes, log):

@@ -172,15 +172,22 @@ class Block:
 
 
 def make_block(cfg: LayerConfig, block: int = 0, layer: int = 0, rho: float = 0.9,
-               T: int | None = None, B: int | None = None) -> Block:
+               T: int | None = None, B: int | None = None, tree_layer: int | None = None) -> Block:
+    """Trees, probabilities, hidden states (and mask) of one verification block.
+
+    tree_layer selects the seed of the tree structure (default: layer); a
+    block seen by every layer of a stack keeps one tree (tree_layer = 0) while
+    each layer draws its own hidden states.
+    """
     T = cfg.T if T is None else T
     B = cfg.B if B is None else B
+    tl = layer if tree_layer is None else tree_layer
     parents, depths, sibs, probs, hid = [], [], [], [], []
     offsets = [0]
     for b in range(B):
-        rt = rng_for(cfg.cfg_id, block, layer * 1000 + b, STREAM_TREE)
+        rt = rng_for(cfg.cfg_id, block, tl * 1000 + b, STREAM_TREE)
         par, dep, sib = make_tree(rt, T, cfg.depth_max, cfg.branch)
-        pr = commit_probs(rng_for(cfg.cfg_id, block, layer * 1000 + b, STREAM_COMMIT),
+        pr = commit_probs(rng_for(cfg.cfg_id, block, tl * 1000 + b, STREAM_COMMIT),
                           cfg.commit_rule, dep, sib)
         hs = correlated_hidden(rng_for(cfg.cfg_id, block, layer * 1000 + b, STREAM_HIDDEN),
                                par, cfg.H, cfg.hidden_std, rho)
