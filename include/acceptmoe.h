@@ -192,8 +192,11 @@ size_t acceptmoe_moe_forward_workspace_size(int32_t T, int32_t H, int32_t I, int
  *   T == 0 is a no-op.
  * bf16: MFMA bf16 products with fp32 accumulation; the SwiGLU activation is
  * rounded to bf16 before the down projection.  fp32: fp32 MFMA throughout.
- * The result is deterministic (the k expert contributions of a token are
- * summed in slot order).
+ * The result is deterministic.  For T <= 256 with T*k <= 2048 the expert
+ * contributions of a token are summed in a fixed expert order inside each of
+ * 8 accumulation lanes, the lanes in a fixed order, and (when I is split in
+ * two) the two fp32 halves added onto zero, which commutes; larger blocks sum
+ * the k contributions of a token in slot order.
  */
 int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_gate,
                               const void* w_up, const void* w_down, int32_t T, int32_t H,

@@ -55,30 +55,74 @@ __device__ __forceinline__ uint64_t lanes_below(int lane) {
 
 __device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
 
-// Butterfly reductions: every lane ends with the same value, and the order of
-// operations is fixed, so results are reproducible run to run.
+// Wave reductions on DPP row operations (no LDS round trips): pairs, quads,
+// half-rows and rows are combined with quad_perm / mirror moves, then rows
+// 0+1 and 2+3 with row_bcast:15 and the two halves with row_bcast:31, leaving
+// the result in lane 63, which is broadcast.  The order of operations is
+// fixed, so sums are reproducible run to run.
+namespace dpp {
+constexpr int kXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kHalfMirror = 0x141; // lane i <-> 7 - i within each 8
+constexpr int kMirror = 0x140;     // lane i <-> 15 - i within each row
+constexpr int kBcast15 = 0x142;    // lane 15 of row r -> row r + 1
+constexpr int kBcast31 = 0x143;    // lane 31 -> rows 2 and 3
+
+// v moved by the DPP control; lanes of rows outside row_mask get `old`
+template <int Ctrl, int RowMask = 0xf>
+__device__ __forceinline__ uint32_t mov(uint32_t old, uint32_t v) {
+  return static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(static_cast<int>(old), static_cast<int>(v), Ctrl, RowMask, 0xf, false));
+}
+template <int Ctrl, int RowMask = 0xf>
+__device__ __forceinline__ float mov(float old, float v) {
+  return __uint_as_float(mov<Ctrl, RowMask>(__float_as_uint(old), __float_as_uint(v)));
+}
+template <int Ctrl, int RowMask = 0xf>
+__device__ __forceinline__ double mov(double old, double v) {
+  const uint64_t o = __double_as_longlong(old), x = __double_as_longlong(v);
+  const uint32_t lo = mov<Ctrl, RowMask>(static_cast<uint32_t>(o), static_cast<uint32_t>(x));
+  const uint32_t hi = mov<Ctrl, RowMask>(static_cast<uint32_t>(o >> 32), static_cast<uint32_t>(x >> 32));
+  return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+
+__device__ __forceinline__ uint32_t lane63(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 63));
+}
+__device__ __forceinline__ float lane63(float v) { return __uint_as_float(lane63(__float_as_uint(v))); }
+__device__ __forceinline__ double lane63(double v) {
+  const uint64_t x = __double_as_longlong(v);
+  const uint64_t lo = lane63(static_cast<uint32_t>(x)), hi = lane63(static_cast<uint32_t>(x >> 32));
+  return __longlong_as_double(static_cast<long long>((hi << 32) | lo));
+}
+
+// op(a, b) must be commutative; id is its identity
+template <class T, class Op>
+__device__ __forceinline__ T reduce(T v, T id, Op op) {
+  v = op(v, mov<kXor1>(id, v));
+  v = op(v, mov<kXor2>(id, v));
+  v = op(v, mov<kHalfMirror>(id, v));
+  v = op(v, mov<kMirror>(id, v));
+  v = op(v, mov<kBcast15, 0xA>(id, v));
+  v = op(v, mov<kBcast31, 0xC>(id, v));
+  return lane63(v);
+}
+}  // namespace dpp
+
 __device__ __forceinline__ double wave_sum_f64(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  return dpp::reduce(v, 0.0, [](double a, double b) { return a + b; });
 }
 
 __device__ __forceinline__ float wave_max_f32(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+  return dpp::reduce(v, -INFINITY, [](float a, float b) { return fmaxf(a, b); });
 }
 
 __device__ __forceinline__ double wave_max_f64(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
-  return v;
+  return dpp::reduce(v, static_cast<double>(-INFINITY), [](double a, double b) { return fmax(a, b); });
 }
 
 __device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  return static_cast<int>(dpp::reduce(static_cast<uint32_t>(v), 0u, [](uint32_t a, uint32_t b) { return a + b; }));
 }
 
 // Orders LDS traffic between the lanes of one wave (no cross-wave barrier).

@@ -6,8 +6,12 @@
 //   gate_up    per (active expert, 16-row tile of I): X_e W_g^T and X_e W_u^T on
 //              MFMA (tokens on the 16-wide M side), SwiGLU in registers, the
 //              activation written once
-//   down       per (active expert, 16-row tile of H): act_e W_d^T, scaled by
-//              the gate and written to the token's slot row
+//   down       blocks of up to kColMaxT tokens: per 16-column tile of H (and
+//              half of I), act_e W_d^T for every dispatched (expert, 16-token
+//              block), scaled by the gates and summed per token in LDS, then
+//              written to out -- no per-slot buffer, no combine pass.
+//              Larger blocks: per (active expert, 16-row tile of H), scaled
+//              rows to the token's slot row, then
 //   combine    out_t = sum over the k slots of token t, in slot order
 //
 // Weights are read in the packed fragment layout (see
@@ -76,6 +80,8 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParam
   __shared__ int s_cnt[kMaxExperts];
   __shared__ int s_off[kMaxExperts + 1];
   __shared__ int s_run[kMaxExperts];
+  __shared__ int s_active[kMaxExperts];
+  __shared__ int s_nact;
   __shared__ uint32_t s_mask[kMaxExperts * (kDispatchChunk / 32)];
   const int tid = threadIdx.x;
   const int E = p.E, k = p.k, T = p.T;
@@ -107,16 +113,42 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParam
       }
       if (e < E) s_off[e] = base + incl - c;
       const uint64_t am = __ballot(c > 0);
-      if (c > 0) p.active[abase + popc64(am & lanes_below(tid))] = e;
+      if (c > 0) {
+        const int pos = abase + popc64(am & lanes_below(tid));
+        p.active[pos] = e;
+        s_active[pos] = e;
+      }
       abase += popc64(am);
       base += __shfl(incl, kWave - 1, kWave);
     }
     if (tid == 0) {
       s_off[E] = base;
+      s_nact = abase;
       *p.n_active = abase;
     }
   }
   __syncthreads();
+  if (p.items != nullptr && tid < kWave) {
+    // down-pass items: (expert, first CSR row, rows) per 16-token block of
+    // each active expert, in active-expert order
+    const int na = s_nact;
+    int base = 0;
+    for (int a0 = 0; a0 < na; a0 += kWave) {
+      const int a = a0 + tid;
+      const int e = a < na ? s_active[a] : 0;
+      const int c = a < na ? s_cnt[e] : 0;
+      const int nb = (c + 15) / 16;
+      int incl = nb;
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int v = __shfl_up(incl, o, kWave);
+        if (tid >= o) incl += v;
+      }
+      for (int m = 0; m < nb; ++m)
+        p.items[base + incl - nb + m] = make_int4(e, s_off[e] + 16 * m, min(16, c - 16 * m), 0);
+      base += __shfl(incl, kWave - 1, kWave);
+    }
+    if (tid == 0) *p.n_items = base;
+  }
   for (int e = tid; e < E; e += kDispatchThreads) {
     p.cnt[e] = s_cnt[e];
     p.off[e] = s_off[e];
@@ -552,6 +584,14 @@ __global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
   const int wg_per_expert = (ntiles + tpw - 1) / tpw;
   const int a = blockIdx.x / wg_per_expert;
   const int tile_base = (blockIdx.x % wg_per_expert) * tpw;
+  if (F == Proj::GateUp && p.zero_out) {
+    // the column-tile down pass adds its two halves of I into out
+    float4* o4 = reinterpret_cast<float4*>(p.out);
+    const size_t n4 = static_cast<size_t>(p.T) * p.H / 4;
+    for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n4;
+         i += static_cast<size_t>(gridDim.x) * blockDim.x)
+      o4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   if (a >= *p.n_active) return;
   const int e = p.active[a];
   const int n_e = p.cnt[e];
@@ -562,6 +602,144 @@ __global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
     else if (MTMAX >= 2 && nmt == 2) ffn_pass<P, F, (MTMAX >= 2 ? 2 : 1), NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
     else if (MTMAX >= 3 && nmt == 3) ffn_pass<P, F, (MTMAX >= 3 ? 3 : 1), NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
     else ffn_pass<P, F, MTMAX, NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Column-tile down pass (blocks of up to kColMaxT tokens).  A workgroup owns
+// one 16-column tile of H and one of `ksplit` (1 or 2) parts of I.  It
+// streams that tile's rows of W_d for every down item (expert e, 16-token
+// block of e's list): the items are dealt round-robin to the waves, and each
+// wave runs one continuous two-stage load pipeline across its items.  After
+// an item's last stage the wave adds gate * (act_e W_d^T) into its own LDS
+// accumulator out_w[t, 16 columns] (a token appears once per expert, so the
+// lanes of one item never collide).  At the end the waves' accumulators are
+// summed in wave order and written to out, or added into the zeroed out when
+// I is split in two (two fp32 additions onto zero commute, so the result
+// does not depend on which half lands first).  Every workgroup does the same
+// work; its LDS footprint keeps it alone on its CU.
+// ---------------------------------------------------------------------------
+constexpr int kColWaves = 8;
+constexpr int kColMaxT = 256;
+constexpr int kColMaxSlots = 2048;
+constexpr int kColMaxItems = kMaxExperts + kColMaxSlots / 16;
+
+struct ColShared {
+  float acc[kColWaves][kColMaxT * 16];  // per-wave token accumulators
+  int tok[kColMaxSlots];                // CSR row -> token
+  float gw[kColMaxSlots];               // CSR row -> gate of that slot
+  int4 items[kColMaxItems];
+};
+
+template <class P, int kU>
+__global__ __launch_bounds__(kColWaves * kWave) void down_col_kernel(ForwardParams p, int ksplit) {
+  __shared__ ColShared sh;
+  const int tid = threadIdx.x;
+  const int wave = wave_id(), lane = lane_id();
+  const int r = lane & 15, g = lane >> 4;
+  const int T = p.T, H = p.H, k = p.k;
+  const int ntiles = H / 16;
+  const int ht = blockIdx.x % ntiles, part = blockIdx.x / ntiles;
+  const int KC = p.I / P::kKF;
+  const int kc0 = part * KC / ksplit;
+  const int L = (KC / ksplit) / kU;  // pipeline stages per item
+  const int rowq = p.I * P::kElemBytes / 16;
+  const int n_items = *p.n_items;
+  const int n_rows = p.off[p.E];
+  for (int i = tid; i < kColWaves * T * 16; i += kColWaves * kWave) sh.acc[i / (T * 16)][i % (T * 16)] = 0.f;
+  for (int i = tid; i < n_rows; i += kColWaves * kWave) {
+    const int slot = p.ent_slot[i];
+    sh.tok[i] = slot / k;
+    sh.gw[i] = p.topk_gate[slot];
+  }
+  for (int i = tid; i < n_items; i += kColWaves * kWave) sh.items[i] = p.items[i];
+  __syncthreads();
+
+  const uint4* wd = static_cast<const uint4*>(p.w_down);
+  const uint4* act = static_cast<const uint4*>(p.act);
+  float* accw = sh.acc[wave];
+  // items wave, wave + W, ...; stage = (item, q), q in [0, L)
+  const int my_items = n_items > wave ? (n_items - wave + kColWaves - 1) / kColWaves : 0;
+  const int nst = my_items * L;
+  struct Cursor {
+    int it, q, e, row0, nrows;
+  };
+  auto fetch = [&](Cursor& c) {
+    if (c.it < n_items) {
+      const int4 d = sh.items[c.it];
+      c.e = d.x;
+      c.row0 = d.y;
+      c.nrows = d.z;
+    }
+  };
+  auto advance = [&](Cursor& c) {
+    if (++c.q == L) {
+      c.q = 0;
+      c.it += kColWaves;
+      fetch(c);
+    }
+  };
+  uint4 w0[kU], x0[kU], w1[kU], x1[kU];
+  auto load = [&](uint4 (&wv)[kU], uint4 (&xv)[kU], const Cursor& c) {
+    const int kc = kc0 + c.q * kU;
+    const uint4* wp = wd + ((static_cast<size_t>(c.e) * ntiles + ht) * KC + kc) * kWave + lane;
+    const uint4* xp = act + static_cast<size_t>(c.row0 + min(r, c.nrows - 1)) * rowq + g + kc * 4;
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      wv[u] = load_weight(wp + u * kWave);
+      xv[u] = xp[u * 4];
+    }
+  };
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](uint4 (&wv)[kU], uint4 (&xv)[kU], Cursor& c) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) acc = P::mma(xv[u], wv[u], acc);
+    if (c.q == L - 1) {
+      // item done: out_w[t] += gate * row, rows 4g..4g+3 of the block, column r
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = 4 * g + i;
+        if (m < c.nrows) {
+          const int row = c.row0 + m;
+          accw[sh.tok[row] * 16 + r] += sh.gw[row] * acc[i];
+        }
+      }
+      acc = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    advance(c);
+  };
+  if (nst > 0) {
+    Cursor lc{wave, 0, 0, 0, 0}, cc{wave, 0, 0, 0, 0};
+    fetch(lc);
+    fetch(cc);
+    load(w0, x0, lc);
+    advance(lc);
+    int st = 0;
+    for (; st + 2 < nst; st += 2) {
+      load(w1, x1, lc);
+      advance(lc);
+      compute(w0, x0, cc);
+      load(w0, x0, lc);
+      advance(lc);
+      compute(w1, x1, cc);
+    }
+    if (st + 1 < nst) {
+      load(w1, x1, lc);
+      compute(w0, x0, cc);
+      compute(w1, x1, cc);
+    } else {
+      compute(w0, x0, cc);
+    }
+  }
+  __syncthreads();
+  // fixed-order sum over the waves, then out (or out += for a half of I)
+  for (int i = tid; i < T * 16; i += kColWaves * kWave) {
+    float v = sh.acc[0][i];
+#pragma unroll
+    for (int w = 1; w < kColWaves; ++w) v += sh.acc[w][i];
+    float* o = p.out + static_cast<size_t>(i >> 4) * H + ht * 16 + (i & 15);
+    if (ksplit == 2) atomicAdd(o, v);
+    else *o = v;
   }
 }
 
@@ -598,15 +776,45 @@ __global__ __launch_bounds__(256) void combine_kernel(ForwardParams p) {
 }
 
 template <class P, int MTMAX>
-hipError_t launch_ffn(const ForwardParams& p, int cap, hipStream_t stream) {
+hipError_t launch_gate_up(const ForwardParams& p, int cap, hipStream_t stream) {
   constexpr int gt = ProjShape<Proj::GateUp, AMOE_GU_NTW, AMOE_GU_KS>::kTilesPerWG;
-  constexpr int dt = ProjShape<Proj::Down, AMOE_DN_NTW, AMOE_DN_KS>::kTilesPerWG;
   const int gu_wg = (p.I / 16 + gt - 1) / gt;
-  const int dn_wg = (p.H / 16 + dt - 1) / dt;
   ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS><<<dim3(cap * gu_wg), 256, 0, stream>>>(p);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  return hipGetLastError();
+}
+
+template <class P, int MTMAX>
+hipError_t launch_down_rows(const ForwardParams& p, int cap, hipStream_t stream) {
+  constexpr int dt = ProjShape<Proj::Down, AMOE_DN_NTW, AMOE_DN_KS>::kTilesPerWG;
+  const int dn_wg = (p.H / 16 + dt - 1) / dt;
   ffn_kernel<P, Proj::Down, MTMAX, AMOE_DN_NTW, AMOE_DN_KS><<<dim3(cap * dn_wg), 256, 0, stream>>>(p);
+  return hipGetLastError();
+}
+
+// Column-tile down pass shape: I split in two when H has at most 128 column
+// tiles (so about 256 workgroups run), k-steps per pipeline stage dividing
+// the part of I.
+struct ColShape {
+  int ksplit, ku;
+};
+
+ColShape col_shape(int H, int I, int is_bf16) {
+  const int KC = I / (is_bf16 ? Bf16Path::kKF : F32Path::kKF);
+  ColShape c;
+  c.ksplit = (H / 16 <= 128 && KC % 2 == 0) ? 2 : 1;
+  const int len = KC / c.ksplit;
+  c.ku = len % 4 == 0 ? 4 : (len % 2 == 0 ? 2 : 1);
+  return c;
+}
+
+bool use_col_path(int T, int k) { return T <= kColMaxT && static_cast<long long>(T) * k <= kColMaxSlots; }
+
+template <class P>
+hipError_t launch_down_col(const ForwardParams& p, const ColShape& c, hipStream_t stream) {
+  const dim3 grid((p.H / 16) * c.ksplit);
+  if (c.ku == 4) down_col_kernel<P, 4><<<grid, kColWaves * kWave, 0, stream>>>(p, c.ksplit);
+  else if (c.ku == 2) down_col_kernel<P, 2><<<grid, kColWaves * kWave, 0, stream>>>(p, c.ksplit);
+  else down_col_kernel<P, 1><<<grid, kColWaves * kWave, 0, stream>>>(p, c.ksplit);
   return hipGetLastError();
 }
 
@@ -623,11 +831,19 @@ hipError_t launch_pack(const void* src, int is_bf16, int E, int N, int K, void* 
   return hipGetLastError();
 }
 
+// workspace: [cnt E | off E+1 | active E | n_active | n_items] ints, CSR slot
+// ids, activations, then the per-slot output rows (row pass) or the down
+// items (column-tile pass)
 size_t forward_workspace_bytes(int T, int H, int I, int E, int k, int is_bf16) {
   const size_t slots = static_cast<size_t>(T) * k;
   const size_t eb = is_bf16 ? 2 : 4;
-  return align256(sizeof(int32_t) * (3 * static_cast<size_t>(E) + 2)) + align256(sizeof(int32_t) * slots) +
-         align256(slots * I * eb) + align256(slots * H * sizeof(float));
+  const size_t head = align256(sizeof(int32_t) * (3 * static_cast<size_t>(E) + 3)) +
+                      align256(sizeof(int32_t) * slots) + align256(slots * I * eb);
+  if (use_col_path(T, k)) {
+    const size_t items = (slots + 15) / 16 + (static_cast<size_t>(E) < slots ? E : slots);
+    return head + align256(items * sizeof(int4));
+  }
+  return head + align256(slots * H * sizeof(float));
 }
 
 void forward_carve(void* ws, ForwardParams& p) {
@@ -639,15 +855,25 @@ void forward_carve(void* ws, ForwardParams& p) {
   p.off = ints + p.E;
   p.active = ints + 2 * p.E + 1;
   p.n_active = ints + 3 * p.E + 1;
-  c += align256(sizeof(int32_t) * (3 * static_cast<size_t>(p.E) + 2));
+  p.n_items = ints + 3 * p.E + 2;
+  c += align256(sizeof(int32_t) * (3 * static_cast<size_t>(p.E) + 3));
   p.ent_slot = reinterpret_cast<int32_t*>(c);
   c += align256(sizeof(int32_t) * slots);
   p.act = c;
   c += align256(slots * p.I * eb);
-  p.ys = reinterpret_cast<float*>(c);
+  if (use_col_path(p.T, p.k)) {
+    p.items = reinterpret_cast<int4*>(c);
+    p.ys = nullptr;
+  } else {
+    p.items = nullptr;
+    p.ys = reinterpret_cast<float*>(c);
+  }
 }
 
-hipError_t launch_forward(const ForwardParams& p, hipStream_t stream) {
+hipError_t launch_forward(ForwardParams p, hipStream_t stream) {
+  const bool col = use_col_path(p.T, p.k);
+  const ColShape cs = col_shape(p.H, p.I, p.is_bf16);
+  p.zero_out = col && cs.ksplit == 2;
   const bool small_k = p.k <= 8;
   if (small_k)
     dispatch_kernel<8><<<1, kDispatchThreads, 0, stream>>>(p);
@@ -657,11 +883,17 @@ hipError_t launch_forward(const ForwardParams& p, hipStream_t stream) {
   if (err != hipSuccess) return err;
   // upper bound on active experts: min(E, T*k)
   const int cap = p.E < p.T * p.k ? p.E : p.T * p.k;
-  if (p.is_bf16) {
-    err = p.T <= 32 ? launch_ffn<Bf16Path, 2>(p, cap, stream) : launch_ffn<Bf16Path, 4>(p, cap, stream);
-  } else {
-    err = p.T <= 32 ? launch_ffn<F32Path, 2>(p, cap, stream) : launch_ffn<F32Path, 4>(p, cap, stream);
-  }
+  const bool small_t = p.T <= 32;
+  if (p.is_bf16)
+    err = small_t ? launch_gate_up<Bf16Path, 2>(p, cap, stream) : launch_gate_up<Bf16Path, 4>(p, cap, stream);
+  else
+    err = small_t ? launch_gate_up<F32Path, 2>(p, cap, stream) : launch_gate_up<F32Path, 4>(p, cap, stream);
+  if (err != hipSuccess) return err;
+  if (col) return p.is_bf16 ? launch_down_col<Bf16Path>(p, cs, stream) : launch_down_col<F32Path>(p, cs, stream);
+  if (p.is_bf16)
+    err = small_t ? launch_down_rows<Bf16Path, 2>(p, cap, stream) : launch_down_rows<Bf16Path, 4>(p, cap, stream);
+  else
+    err = small_t ? launch_down_rows<F32Path, 2>(p, cap, stream) : launch_down_rows<F32Path, 4>(p, cap, stream);
   if (err != hipSuccess) return err;
   dim3 cgrid((p.H / 4 + 255) / 256, p.T);
   if (small_k)

@@ -64,12 +64,15 @@ struct ForwardParams {
   int32_t* n_active;  // [1]
   int32_t* ent_slot;  // [T * k] slot ids grouped by expert, token order
   void* act;          // [T * k, I] bf16 or fp32
-  float* ys;          // [T * k, H] gate-weighted expert outputs
+  float* ys;          // [T * k, H] gate-weighted expert outputs (per-slot down pass only)
+  int4* items;        // down-pass work items (e, first CSR row, rows) (column-tile pass only)
+  int32_t* n_items;   // [1]
   int T, H, I, E, k, is_bf16;
+  int zero_out;       // gate/up pass clears out (the down pass then adds two halves into it)
 };
 
 size_t forward_workspace_bytes(int T, int H, int I, int E, int k, int is_bf16);
 void forward_carve(void* ws, ForwardParams& p);
-hipError_t launch_forward(const ForwardParams& p, hipStream_t stream);
+hipError_t launch_forward(ForwardParams p, hipStream_t stream);
 
 }  // namespace amoe

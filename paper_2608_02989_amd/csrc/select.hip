@@ -1,17 +1,20 @@
-// AcceptMoE eligible-set selection as three kernels.
+// AcceptMoE eligible-set selection.
 //
-//   natural_kernel    one wave per node, spread over many CUs: natural top-k
-//                     K_t over the fp32 logits and r_t = softmax(z_t) in fp64
-//                     for the selected experts                  (Sec. 3.1, Eq. 1)
-//   tree_kernel       one 1024-thread workgroup per draft tree:
+//   natural top-k     per node: K_t over the fp32 logits and r_t = softmax(z_t)
+//                     in fp64 for the selected experts           (Sec. 3.1, Eq. 1)
+//   tree stage        per draft tree:
 //     P1  depth / parent / probability of every node; tree checks, depth
 //         counts N_d, importance alpha_t = p_t^beta / sqrt(N_{d_t})   (Eq. 3)
 //     P3  utility u_e = sum_t alpha_t r_{t,e} 1[e in K_t], summed in node order
 //         through a dense LDS tile; votes v_e; root anchor A         (Eq. 4, Eq. 5)
 //     P4  effective rank over R = [E] \ A, self-sized set S, optional
 //         residency pruning -> S'                        (Eq. 6, Sec. 3.3, Eq. 7)
-//   restricted_kernel one wave per node: restricted top-k over S' and
-//                     renormalised gates                                  (Eq. 2)
+//   restricted top-k  per node: top-k over S' and renormalised gates   (Eq. 2)
+//
+// Three launches: natural_kernel and restricted_kernel put one wave on each
+// node and spread the nodes over many CUs (the per-node work is bound by
+// instruction issue, so it needs the SIMDs of many CUs); tree_kernel runs one
+// 1024-thread workgroup per tree between them.
 //
 // Top-k is a wave-wide radix select on order-preserving 32-bit keys: the k-th
 // largest key is found bit by bit with ballots, keys above it are taken,
@@ -56,11 +59,14 @@ struct SelShared {
 };
 
 // per-wave compaction scratch for top-k slot ordering
-struct NodeScratch {
-  alignas(16) uint32_t sk[kNodeWaves][kMaxTopK];
-  alignas(16) int se[kNodeWaves][kMaxTopK];
-  alignas(16) float sz[kNodeWaves][kMaxTopK];
+template <int W>
+struct NodeScratchT {
+  alignas(16) uint32_t sk[W][kMaxTopK];
+  alignas(16) int se[W][kMaxTopK];
+  alignas(16) float sz[W][kMaxTopK];
+  alignas(16) double sx[W][kMaxTopK];
 };
+typedef NodeScratchT<kNodeWaves> NodeScratch;
 
 // k-th largest key among the wave's EPL*64 keys (0 if fewer than k are non-zero).
 template <int EPL>
@@ -77,11 +83,12 @@ __device__ __forceinline__ uint32_t kth_largest(const uint32_t (&key)[EPL], int 
 }
 
 // Selects the top-k keys of the wave (ties -> lower expert index) and
-// compacts the winners into the wave's scratch in expert-index order.
+// compacts the winners into the wave's scratch in expert-index order: key and
+// expert index, plus put(pos, i) for the caller's own payload of element i.
 // Returns the number selected (min(k, #non-zero keys)).
-template <int EPL>
-__device__ __forceinline__ int wave_topk_compact(const uint32_t (&key)[EPL], const float (&zv)[EPL],
-                                                 int k, int lane, uint32_t* sk, int* se, float* sz) {
+template <int EPL, class Put>
+__device__ __forceinline__ int wave_topk_compact(const uint32_t (&key)[EPL], int k, int lane, uint32_t* sk,
+                                                 int* se, Put&& put) {
   const uint32_t thr = kth_largest<EPL>(key, k);
   int greater = 0;
 #pragma unroll
@@ -100,7 +107,7 @@ __device__ __forceinline__ int wave_topk_compact(const uint32_t (&key)[EPL], con
       const int pos = base + popc64(sm & below);
       sk[pos] = key[i];
       se[pos] = lane + kWave * i;
-      sz[pos] = zv[i];
+      put(pos, i);
     }
     base += popc64(sm);
   }
@@ -191,14 +198,11 @@ __device__ __forceinline__ void load_row(const float* __restrict__ zrow, int E, 
 }
 
 // ---------------------------------------------------------------------------
-// natural top-k and router probabilities, one wave per node
+// natural top-k and router probabilities of node t (one wave)
 // ---------------------------------------------------------------------------
 template <int EPL>
-__global__ __launch_bounds__(kNodeWaves * kWave) void natural_kernel(SelectParams p) {
-  __shared__ NodeScratch ns;
-  const int wave = wave_id(), lane = lane_id();
-  const int t = blockIdx.x * kNodeWaves + wave;
-  if (t >= p.T) return;
+__device__ __forceinline__ void natural_node(const SelectParams& p, int t, int lane, uint32_t* sk, int* se,
+                                             double* sx) {
   const int E = p.E, k = p.k;
   float zv[EPL];
   uint32_t key[EPL];
@@ -225,16 +229,65 @@ __global__ __launch_bounds__(kNodeWaves * kWave) void natural_kernel(SelectParam
       if (e < E) p.ws_rfull[static_cast<size_t>(t) * E + e] = ex[i] / den;
     }
   }
-  uint32_t* sk = ns.sk[wave];
-  int* se = ns.se[wave];
-  float* sz = ns.sz[wave];
-  const int n = wave_topk_compact<EPL>(key, zv, k, lane, sk, se, sz);
+  const int n = wave_topk_compact<EPL>(key, k, lane, sk, se, [&](int pos, int i) { sx[pos] = ex[i]; });
   if (lane < n) {
     const int slot = slot_of(lane, n, sk, se);
     p.ws_kidx[static_cast<size_t>(t) * k + slot] = se[lane];
-    p.ws_r[static_cast<size_t>(t) * k + slot] =
-        exp(static_cast<double>(sz[lane]) - static_cast<double>(zmax)) / den;
+    p.ws_r[static_cast<size_t>(t) * k + slot] = sx[lane] / den;
   }
+  wave_lds_sync();  // the scratch is reused by the wave's next node
+}
+
+template <int EPL>
+__global__ __launch_bounds__(kNodeWaves * kWave) void natural_kernel(SelectParams p) {
+  __shared__ NodeScratch ns;
+  const int wave = wave_id(), lane = lane_id();
+  const int t = blockIdx.x * kNodeWaves + wave;
+  if (t >= p.T) return;
+  natural_node<EPL>(p, t, lane, ns.sk[wave], ns.se[wave], ns.sx[wave]);
+}
+
+// ---------------------------------------------------------------------------
+// restricted top-k over the eligible set and renormalised gates of node t
+// (one wave).  elig[e] != 0 marks e in S'.  Experts that receive the node are
+// counted into stats[b][9] once each, through the tree's bitmask in the
+// workspace.
+// ---------------------------------------------------------------------------
+template <int EPL>
+__device__ __forceinline__ void restricted_node(const SelectParams& p, int t, int b, const uint8_t* elig, int lane,
+                                                uint32_t* sk, int* se, float* sz) {
+  const int E = p.E, k = p.k;
+  float zv[EPL];
+  uint32_t key[EPL];
+  load_row<EPL>(p.logits + static_cast<size_t>(t) * E, E, lane, zv);
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + kWave * i;
+    key[i] = (e < E && elig[e]) ? logit_key(zv[i]) : 0u;
+  }
+  const int n = wave_topk_compact<EPL>(key, k, lane, sk, se, [&](int pos, int i) { sz[pos] = zv[i]; });
+  // gates: softmax over the selected logits, fp64
+  double zm = lane < n ? static_cast<double>(sz[lane]) : -INFINITY;
+  zm = wave_max_f64(zm);
+  const double w = lane < n ? exp(static_cast<double>(sz[lane]) - zm) : 0.0;
+  const double ws = wave_sum_f64(w);
+  int32_t* orow = p.topk_idx + static_cast<size_t>(t) * k;
+  float* grow = p.topk_gate + static_cast<size_t>(t) * k;
+  if (lane < n) {
+    const int slot = slot_of(lane, n, sk, se);
+    const int e = se[lane];
+    orow[slot] = e;
+    grow[slot] = static_cast<float>(w / ws);
+    if (p.stats != nullptr) {
+      const uint32_t bit = 1u << (e & 31);
+      const uint32_t old = atomicOr(&p.ws_routed[b * kRoutedWords + (e >> 5)], bit);
+      if (!(old & bit)) atomicAdd(&p.stats[b * kNumStats + 9], 1);
+    }
+  } else if (lane < k) {
+    orow[lane] = -1;  // fewer eligible experts than k (an invalid tree has none)
+    grow[lane] = 0.0f;
+  }
+  wave_lds_sync();  // the scratch is reused by the wave's next node
 }
 
 // ---------------------------------------------------------------------------
@@ -493,7 +546,7 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
 }
 
 // ---------------------------------------------------------------------------
-// restricted top-k over S' and renormalised gates, one wave per node
+// restricted top-k, one wave per node
 // ---------------------------------------------------------------------------
 template <int EPL>
 __global__ __launch_bounds__(kNodeWaves * kWave) void restricted_kernel(SelectParams p, TreeOffsets offs) {
@@ -501,7 +554,6 @@ __global__ __launch_bounds__(kNodeWaves * kWave) void restricted_kernel(SelectPa
   const int wave = wave_id(), lane = lane_id();
   const int t = blockIdx.x * kNodeWaves + wave;
   if (t >= p.T) return;
-  const int E = p.E, k = p.k;
   // tree of node t: the b with o[b] <= t < o[b+1] (empty trees are skipped)
   int lo = 0, hi = p.B - 1;
   while (lo < hi) {
@@ -509,41 +561,8 @@ __global__ __launch_bounds__(kNodeWaves * kWave) void restricted_kernel(SelectPa
     if (offs.o[mid] <= t) lo = mid;
     else hi = mid - 1;
   }
-  const int b = lo;
-  const uint8_t* elig = p.eligible + static_cast<size_t>(b) * E;
-  float zv[EPL];
-  uint32_t key[EPL];
-  load_row<EPL>(p.logits + static_cast<size_t>(t) * E, E, lane, zv);
-#pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    const int e = lane + kWave * i;
-    key[i] = (e < E && elig[e]) ? logit_key(zv[i]) : 0u;
-  }
-  uint32_t* sk = ns.sk[wave];
-  int* se = ns.se[wave];
-  float* sz = ns.sz[wave];
-  const int n = wave_topk_compact<EPL>(key, zv, k, lane, sk, se, sz);
-  // gates: softmax over the selected logits, fp64
-  double zm = lane < n ? static_cast<double>(sz[lane]) : -INFINITY;
-  zm = wave_max_f64(zm);
-  const double w = lane < n ? exp(static_cast<double>(sz[lane]) - zm) : 0.0;
-  const double ws = wave_sum_f64(w);
-  int32_t* orow = p.topk_idx + static_cast<size_t>(t) * k;
-  float* grow = p.topk_gate + static_cast<size_t>(t) * k;
-  if (lane < n) {
-    const int slot = slot_of(lane, n, sk, se);
-    const int e = se[lane];
-    orow[slot] = e;
-    grow[slot] = static_cast<float>(w / ws);
-    if (p.stats != nullptr) {
-      const uint32_t bit = 1u << (e & 31);
-      const uint32_t old = atomicOr(&p.ws_routed[b * kRoutedWords + (e >> 5)], bit);
-      if (!(old & bit)) atomicAdd(&p.stats[b * kNumStats + 9], 1);
-    }
-  } else if (lane < k) {
-    orow[lane] = -1;  // fewer eligible experts than k (an invalid tree has none)
-    grow[lane] = 0.0f;
-  }
+  restricted_node<EPL>(p, t, lo, p.eligible + static_cast<size_t>(lo) * p.E, lane, ns.sk[wave], ns.se[wave],
+                       ns.sz[wave]);
 }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }

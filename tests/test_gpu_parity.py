@@ -194,10 +194,12 @@ def test_select_parity_root_only_and_ties(gpu):
     assert_select_equal(got, ref, "repeated")
 
 
-def test_select_parity_batch_with_invalid_trees(gpu):
+# a batch of small, empty and invalid trees, with and without a tree of more
+# than 64 nodes
+@pytest.mark.parametrize("sizes", [[64, 1, 0, 17, 64, 5, 33], [100, 1, 0, 17, 64, 5, 33]])
+def test_select_parity_batch_with_invalid_trees(gpu, sizes):
     rng = np.random.default_rng(9)
     E, k = 128, 8
-    sizes = [64, 1, 0, 17, 64, 5, 33]
     pars, deps, probs = [], [], []
     offs = [0]
     for s in sizes:
@@ -263,23 +265,23 @@ def test_forward_parity_batched_sampled(gpu):
     assert np.isfinite(got).all()
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_forward_parity_ragged_and_hot_expert(gpu, dtype):
+# T = 100 takes the column-tile down pass, T = 300 the per-slot pass + combine
+@pytest.mark.parametrize("dtype,T", [("bf16", 100), ("f32", 100), ("bf16", 300), ("f32", 300)])
+def test_forward_parity_ragged_and_hot_expert(gpu, dtype, T):
     # T not a multiple of 16, E not a multiple of 64, one expert receiving every token
-    cfg = W.LayerConfig("ragged", 90 + (dtype == "f32"), dtype, T=100, B=1, H=256, E=20, k=3, I=96,
+    cfg = W.LayerConfig("ragged", 90 + (dtype == "f32"), dtype, T=T, B=1, H=256, E=20, k=3, I=96,
                         depth_max=6, commit_rule="depth_sibling", hidden_std=1.0)
     rng = np.random.default_rng(3)
-    T = 100
     h32 = rng.standard_normal((T, cfg.H)).astype(np.float32)
     others = np.array([e for e in range(cfg.E) if e != 7])
-    # expert 7 gets all 100 tokens (several 64-token passes); the rest distinct per row
+    # expert 7 gets every token (several 64-token passes); the rest distinct per row
     idx = np.stack([np.concatenate([[7], rng.permutation(others)[:cfg.k - 1]]) for _ in range(T)])
     idx = idx.astype(np.int32)
     idx[5] = [3, -1, 25]                            # invalid entries are skipped
     idx[6] = [-1, -1, -1]                           # no expert at all -> zero row
     idx[9] = [4, 11, 4]                             # a repeated expert counts once (first slot)
     gate = rng.random((T, cfg.k)).astype(np.float32)
-    say(f"forward ragged dtype={dtype}")
+    say(f"forward ragged dtype={dtype} T={T}")
     got, h64, (wg, wu, wd) = forward_case(cfg, idx, gate, h32)
     clean = np.where((idx >= 0) & (idx < cfg.E), idx, -1)
     clean[9, 2] = -1
