@@ -69,6 +69,55 @@ __device__ __forceinline__ uint32_t load_route_row(const int32_t* __restrict__ r
   return valid;
 }
 
+// Exclusive scan of per-expert counts and compaction of the active experts,
+// in index order (one wave, lane = tid < 64).  Returns the number of active
+// experts; off[E] = total dispatched slots.
+__device__ __forceinline__ int scan_experts(const int* cnt, int* off, int* active, int* active_g, int E, int tid) {
+  int base = 0, abase = 0;
+  for (int e0 = 0; e0 < E; e0 += kWave) {
+    const int e = e0 + tid;
+    const int c = e < E ? cnt[e] : 0;
+    int incl = c;
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int v = __shfl_up(incl, o, kWave);
+      if (tid >= o) incl += v;
+    }
+    if (e < E) off[e] = base + incl - c;
+    const uint64_t am = __ballot(c > 0);
+    if (c > 0) {
+      const int pos = abase + popc64(am & lanes_below(tid));
+      active[pos] = e;
+      if (active_g != nullptr) active_g[pos] = e;
+    }
+    abase += popc64(am);
+    base += __shfl(incl, kWave - 1, kWave);
+  }
+  if (tid == 0) off[E] = base;
+  return abase;
+}
+
+// Down-pass items (expert, first CSR row, rows) per 16-token block of each
+// active expert, in active-expert order, and their count (one wave).
+__device__ __forceinline__ void write_down_items(const ForwardParams& p, const int* cnt, const int* off,
+                                                 const int* active, int na, int tid) {
+  int base = 0;
+  for (int a0 = 0; a0 < na; a0 += kWave) {
+    const int a = a0 + tid;
+    const int e = a < na ? active[a] : 0;
+    const int c = a < na ? cnt[e] : 0;
+    const int nb = (c + 15) / 16;
+    int incl = nb;
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int v = __shfl_up(incl, o, kWave);
+      if (tid >= o) incl += v;
+    }
+    for (int m = 0; m < nb; ++m)
+      p.items[base + incl - nb + m] = make_int4(e, off[e] + 16 * m, min(16, c - 16 * m), 0);
+    base += __shfl(incl, kWave - 1, kWave);
+  }
+  if (tid == 0) *p.n_items = base;
+}
+
 // ---------------------------------------------------------------------------
 // dispatch: CSR of (expert -> slot ids in node order), active expert list.
 // One workgroup; each thread owns one node per pass and keeps its row in
@@ -101,54 +150,14 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParam
   }
   __syncthreads();
   if (tid < kWave) {
-    // exclusive scan over experts and compaction of active ones, in index order
-    int base = 0, abase = 0;
-    for (int e0 = 0; e0 < E; e0 += kWave) {
-      const int e = e0 + tid;
-      const int c = e < E ? s_cnt[e] : 0;
-      int incl = c;
-      for (int o = 1; o < kWave; o <<= 1) {
-        const int v = __shfl_up(incl, o, kWave);
-        if (tid >= o) incl += v;
-      }
-      if (e < E) s_off[e] = base + incl - c;
-      const uint64_t am = __ballot(c > 0);
-      if (c > 0) {
-        const int pos = abase + popc64(am & lanes_below(tid));
-        p.active[pos] = e;
-        s_active[pos] = e;
-      }
-      abase += popc64(am);
-      base += __shfl(incl, kWave - 1, kWave);
-    }
+    const int na = scan_experts(s_cnt, s_off, s_active, p.active, E, tid);
     if (tid == 0) {
-      s_off[E] = base;
-      s_nact = abase;
-      *p.n_active = abase;
+      s_nact = na;
+      *p.n_active = na;
     }
   }
   __syncthreads();
-  if (p.items != nullptr && tid < kWave) {
-    // down-pass items: (expert, first CSR row, rows) per 16-token block of
-    // each active expert, in active-expert order
-    const int na = s_nact;
-    int base = 0;
-    for (int a0 = 0; a0 < na; a0 += kWave) {
-      const int a = a0 + tid;
-      const int e = a < na ? s_active[a] : 0;
-      const int c = a < na ? s_cnt[e] : 0;
-      const int nb = (c + 15) / 16;
-      int incl = nb;
-      for (int o = 1; o < kWave; o <<= 1) {
-        const int v = __shfl_up(incl, o, kWave);
-        if (tid >= o) incl += v;
-      }
-      for (int m = 0; m < nb; ++m)
-        p.items[base + incl - nb + m] = make_int4(e, s_off[e] + 16 * m, min(16, c - 16 * m), 0);
-      base += __shfl(incl, kWave - 1, kWave);
-    }
-    if (tid == 0) *p.n_items = base;
-  }
+  if (p.items != nullptr && tid < kWave) write_down_items(p, s_cnt, s_off, s_active, s_nact, tid);
   for (int e = tid; e < E; e += kDispatchThreads) {
     p.cnt[e] = s_cnt[e];
     p.off[e] = s_off[e];
@@ -187,6 +196,78 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParam
     }
     __syncthreads();
   }
+}
+
+// ---------------------------------------------------------------------------
+// In-workgroup dispatch for blocks of up to kSelfMaxT tokens: every gate/up
+// workgroup builds the same CSR in LDS from the routing rows (one row per
+// thread), so no separate dispatch launch is needed; workgroup 0 also
+// publishes it (and the down items) for the down pass.
+// ---------------------------------------------------------------------------
+constexpr int kSelfMaxT = 256;
+constexpr int kSelfMaxSlots = 2048;
+constexpr int kSelfWords = kSelfMaxT / 32;
+
+struct SelfDispatch {
+  int cnt[kMaxExperts];
+  int off[kMaxExperts + 1];
+  int active[kMaxExperts];
+  uint32_t mask[kMaxExperts * kSelfWords];  // per-expert token bitmasks
+  int ent[kSelfMaxSlots];                   // CSR: slot ids grouped by expert, token order
+  int nact;
+};
+
+// blockDim.x == 256 >= T
+template <int KMAX>
+__device__ __forceinline__ void self_dispatch(const ForwardParams& p, SelfDispatch& sd, int tid) {
+  const int E = p.E, k = p.k, T = p.T;
+  const int words = (T + 31) / 32;
+  for (int i = tid; i < E; i += 256) sd.cnt[i] = 0;
+  for (int i = tid; i < E * words; i += 256) sd.mask[i] = 0u;
+  __syncthreads();
+  int ev[KMAX];
+  uint32_t valid = 0u;
+  if (tid < T) {
+    valid = load_route_row<KMAX>(p.topk_idx + static_cast<size_t>(tid) * k, k, E, ev);
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (valid & (1u << j)) {
+        atomicAdd(&sd.cnt[ev[j]], 1);
+        atomicOr(&sd.mask[ev[j] * words + (tid >> 5)], 1u << (tid & 31));
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    const int na = scan_experts(sd.cnt, sd.off, sd.active, nullptr, E, tid);
+    if (tid == 0) sd.nact = na;
+  }
+  __syncthreads();
+  if (tid < T) {
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (valid & (1u << j)) {
+        const uint32_t* m = sd.mask + ev[j] * words;
+        int before = __popc(m[tid >> 5] & ((1u << (tid & 31)) - 1u));
+        for (int w = 0; w < (tid >> 5); ++w) before += __popc(m[w]);
+        sd.ent[sd.off[ev[j]] + before] = tid * k + j;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// workgroup 0: CSR, active list and down items to the workspace
+__device__ __forceinline__ void publish_dispatch(const ForwardParams& p, const SelfDispatch& sd, int tid) {
+  const int E = p.E;
+  for (int e = tid; e <= E; e += 256) {
+    p.off[e] = sd.off[e];
+    if (e < E) p.cnt[e] = sd.cnt[e];
+  }
+  for (int i = tid; i < sd.nact; i += 256) p.active[i] = sd.active[i];
+  for (int i = tid; i < sd.off[E]; i += 256) p.ent_slot[i] = sd.ent[i];
+  if (tid == 0) *p.n_active = sd.nact;
+  if (tid < kWave) write_down_items(p, sd.cnt, sd.off, sd.active, sd.nact, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -470,8 +551,8 @@ struct ProjShape {
 };
 
 template <class P, Proj F, int MT, int NTW, int KS>
-__device__ __forceinline__ void ffn_pass(const ForwardParams& p, int e, int tile_base, int n_e, int o_e, int m0,
-                                         floatx4 (*red)[kWave][4], uint4* xs) {
+__device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* ent, int e, int tile_base, int n_e,
+                                         int o_e, int m0, floatx4 (*red)[kWave][4], uint4* xs) {
   constexpr int NB = ProjShape<F, NTW, KS>::kNB;
   const int wave = wave_id(), lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
@@ -485,11 +566,11 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, int e, int tile
   const uint4* x[MT];
   if (F == Proj::GateUp) {
     const uint4* hid = static_cast<const uint4*>(p.hidden);
-    const int tok0 = p.ent_slot[o_e] / p.k;  // rows past n_e read a valid row; their outputs are dropped
+    const int tok0 = ent[o_e] / p.k;  // rows past n_e read a valid row; their outputs are dropped
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int m = m0 + mt * 16 + r;
-      const int tok = m < n_e ? p.ent_slot[o_e + m] / p.k : tok0;
+      const int tok = m < n_e ? ent[o_e + m] / p.k : tok0;
       x[mt] = hid + static_cast<size_t>(tok) * rowq + g;
     }
   } else {
@@ -564,7 +645,7 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, int e, int tile
               else
                 static_cast<float*>(p.act)[idx] = v;
             } else {
-              const int s = p.ent_slot[o_e + m];
+              const int s = ent[o_e + m];
               p.ys[static_cast<size_t>(s) * p.H + tile * 16 + r] = p.topk_gate[s] * acc[j][mt][i];
             }
           }
@@ -574,16 +655,31 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, int e, int tile
   }
 }
 
-// grid.x = cap_experts * ceil(ntiles / tiles_per_wg)
-template <class P, Proj F, int MTMAX, int NTW, int KS>
+template <bool kSelf>
+struct SelfDispatchSlot {
+  SelfDispatch sd;
+};
+template <>
+struct SelfDispatchSlot<false> {
+  int unused;
+};
+
+// Work item i = (active expert i / wg_per_expert, tile run i % wg_per_expert).
+// Without kSelf: grid.x = cap_experts * wg_per_expert, one item per
+// workgroup, reading dispatch_kernel's CSR.  kSelf (gate/up pass, blocks of up
+// to kSelfMaxT tokens): a grid of at most kSelfGrid workgroups (about three
+// per CU, all resident) builds the dispatch in LDS once and takes items
+// blockIdx.x, blockIdx.x + gridDim.x, ...
+constexpr int kSelfGrid = 768;
+
+template <class P, Proj F, int MTMAX, int NTW, int KS, bool kSelf, int KMAX>
 __global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
   __shared__ floatx4 red[KS > 1 ? 4 : 1][kWave][4];
   __shared__ uint4 xs[KS == 1 ? shared_a_pieces<MTMAX>() * kWave : 1];
+  __shared__ SelfDispatchSlot<kSelf> sds;
   constexpr int tpw = ProjShape<F, NTW, KS>::kTilesPerWG;
   const int ntiles = (F == Proj::GateUp ? p.I : p.H) / 16;
   const int wg_per_expert = (ntiles + tpw - 1) / tpw;
-  const int a = blockIdx.x / wg_per_expert;
-  const int tile_base = (blockIdx.x % wg_per_expert) * tpw;
   if (F == Proj::GateUp && p.zero_out) {
     // the column-tile down pass adds its two halves of I into out
     float4* o4 = reinterpret_cast<float4*>(p.out);
@@ -592,16 +688,29 @@ __global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
          i += static_cast<size_t>(gridDim.x) * blockDim.x)
       o4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  if (a >= *p.n_active) return;
-  const int e = p.active[a];
-  const int n_e = p.cnt[e];
-  const int o_e = p.off[e];
-  for (int m0 = 0; m0 < n_e; m0 += 16 * MTMAX) {
-    const int nmt = min(MTMAX, (n_e - m0 + 15) / 16);
-    if (nmt == 1) ffn_pass<P, F, 1, NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
-    else if (MTMAX >= 2 && nmt == 2) ffn_pass<P, F, (MTMAX >= 2 ? 2 : 1), NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
-    else if (MTMAX >= 3 && nmt == 3) ffn_pass<P, F, (MTMAX >= 3 ? 3 : 1), NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
-    else ffn_pass<P, F, MTMAX, NTW, KS>(p, e, tile_base, n_e, o_e, m0, red, xs);
+  auto run_item = [&](int item, const int* active, const int* cnt, const int* off, const int32_t* ent) {
+    const int a = item / wg_per_expert;
+    const int tile_base = (item % wg_per_expert) * tpw;
+    const int e = active[a];
+    const int n_e = cnt[e];
+    const int o_e = off[e];
+    for (int m0 = 0; m0 < n_e; m0 += 16 * MTMAX) {
+      const int nmt = min(MTMAX, (n_e - m0 + 15) / 16);
+      if (nmt == 1) ffn_pass<P, F, 1, NTW, KS>(p, ent, e, tile_base, n_e, o_e, m0, red, xs);
+      else if (MTMAX >= 2 && nmt == 2) ffn_pass<P, F, (MTMAX >= 2 ? 2 : 1), NTW, KS>(p, ent, e, tile_base, n_e, o_e, m0, red, xs);
+      else if (MTMAX >= 3 && nmt == 3) ffn_pass<P, F, (MTMAX >= 3 ? 3 : 1), NTW, KS>(p, ent, e, tile_base, n_e, o_e, m0, red, xs);
+      else ffn_pass<P, F, MTMAX, NTW, KS>(p, ent, e, tile_base, n_e, o_e, m0, red, xs);
+    }
+  };
+  if constexpr (kSelf) {
+    SelfDispatch& sd = sds.sd;
+    self_dispatch<KMAX>(p, sd, threadIdx.x);
+    if (blockIdx.x == 0) publish_dispatch(p, sd, threadIdx.x);
+    const int n_items = sd.nact * wg_per_expert;
+    for (int item = blockIdx.x; item < n_items; item += gridDim.x) run_item(item, sd.active, sd.cnt, sd.off, sd.ent);
+  } else {
+    if (static_cast<int>(blockIdx.x) >= *p.n_active * wg_per_expert) return;
+    run_item(blockIdx.x, p.active, p.cnt, p.off, p.ent_slot);
   }
 }
 
@@ -776,10 +885,16 @@ __global__ __launch_bounds__(256) void combine_kernel(ForwardParams p) {
 }
 
 template <class P, int MTMAX>
-hipError_t launch_gate_up(const ForwardParams& p, int cap, hipStream_t stream) {
+hipError_t launch_gate_up(const ForwardParams& p, int cap, bool self, hipStream_t stream) {
   constexpr int gt = ProjShape<Proj::GateUp, AMOE_GU_NTW, AMOE_GU_KS>::kTilesPerWG;
-  const int gu_wg = (p.I / 16 + gt - 1) / gt;
-  ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS><<<dim3(cap * gu_wg), 256, 0, stream>>>(p);
+  const int items = cap * ((p.I / 16 + gt - 1) / gt);
+  const dim3 grid(self ? (items < kSelfGrid ? items : kSelfGrid) : items);
+  if (!self)
+    ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, false, 8><<<grid, 256, 0, stream>>>(p);
+  else if (p.k <= 8)
+    ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, 8><<<grid, 256, 0, stream>>>(p);
+  else
+    ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, kMaxTopK><<<grid, 256, 0, stream>>>(p);
   return hipGetLastError();
 }
 
@@ -787,7 +902,7 @@ template <class P, int MTMAX>
 hipError_t launch_down_rows(const ForwardParams& p, int cap, hipStream_t stream) {
   constexpr int dt = ProjShape<Proj::Down, AMOE_DN_NTW, AMOE_DN_KS>::kTilesPerWG;
   const int dn_wg = (p.H / 16 + dt - 1) / dt;
-  ffn_kernel<P, Proj::Down, MTMAX, AMOE_DN_NTW, AMOE_DN_KS><<<dim3(cap * dn_wg), 256, 0, stream>>>(p);
+  ffn_kernel<P, Proj::Down, MTMAX, AMOE_DN_NTW, AMOE_DN_KS, false, 8><<<dim3(cap * dn_wg), 256, 0, stream>>>(p);
   return hipGetLastError();
 }
 
@@ -807,7 +922,12 @@ ColShape col_shape(int H, int I, int is_bf16) {
   return c;
 }
 
-bool use_col_path(int T, int k) { return T <= kColMaxT && static_cast<long long>(T) * k <= kColMaxSlots; }
+// blocks of up to 256 tokens and 2048 slots: gate/up builds its own dispatch,
+// the column-tile down pass replaces the per-slot pass and combine
+bool use_col_path(int T, int k) {
+  return T <= kColMaxT && T <= kSelfMaxT && static_cast<long long>(T) * k <= kColMaxSlots &&
+         static_cast<long long>(T) * k <= kSelfMaxSlots;
+}
 
 template <class P>
 hipError_t launch_down_col(const ForwardParams& p, const ColShape& c, hipStream_t stream) {
@@ -875,19 +995,22 @@ hipError_t launch_forward(ForwardParams p, hipStream_t stream) {
   const ColShape cs = col_shape(p.H, p.I, p.is_bf16);
   p.zero_out = col && cs.ksplit == 2;
   const bool small_k = p.k <= 8;
-  if (small_k)
-    dispatch_kernel<8><<<1, kDispatchThreads, 0, stream>>>(p);
-  else
-    dispatch_kernel<kMaxTopK><<<1, kDispatchThreads, 0, stream>>>(p);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  hipError_t err = hipSuccess;
+  if (!col) {
+    if (small_k)
+      dispatch_kernel<8><<<1, kDispatchThreads, 0, stream>>>(p);
+    else
+      dispatch_kernel<kMaxTopK><<<1, kDispatchThreads, 0, stream>>>(p);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
   // upper bound on active experts: min(E, T*k)
   const int cap = p.E < p.T * p.k ? p.E : p.T * p.k;
   const bool small_t = p.T <= 32;
   if (p.is_bf16)
-    err = small_t ? launch_gate_up<Bf16Path, 2>(p, cap, stream) : launch_gate_up<Bf16Path, 4>(p, cap, stream);
+    err = small_t ? launch_gate_up<Bf16Path, 2>(p, cap, col, stream) : launch_gate_up<Bf16Path, 4>(p, cap, col, stream);
   else
-    err = small_t ? launch_gate_up<F32Path, 2>(p, cap, stream) : launch_gate_up<F32Path, 4>(p, cap, stream);
+    err = small_t ? launch_gate_up<F32Path, 2>(p, cap, col, stream) : launch_gate_up<F32Path, 4>(p, cap, col, stream);
   if (err != hipSuccess) return err;
   if (col) return p.is_bf16 ? launch_down_col<Bf16Path>(p, cs, stream) : launch_down_col<F32Path>(p, cs, stream);
   if (p.is_bf16)
