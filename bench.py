@@ -158,7 +158,7 @@ def main():
             return L_.step(B_["h"], B_["parent"], B_["depth"], B_["prob"], B_["offs"], B_["resident"], stream)
         T = B_["h"].shape[0]
         logits = L_.logits[:T]
-        ops.route(B_["h"], L_.router_w, out=logits, stream=stream)
+        ops.route(B_["h"], L_.router, out=logits, stream=stream)
         nb = len(B_["offs"]) - 1
         outs = {"eligible": L_.sel_out["eligible"][:nb], "idx": L_.sel_out["idx"][:T],
                 "gate": L_.sel_out["gate"][:T], "stats": L_.sel_out["stats"][:nb]}
@@ -336,7 +336,7 @@ def stack_report(args, cfg):
     nblocks = args.blocks if args.blocks != 16 else cfg.blocks
     nl = cfg.layers
     T, E, k = cfg.T, cfg.E, cfg.k
-    routers = [torch.from_numpy(W.router_weights(cfg, l)).to(dev) for l in range(nl)]
+    routers = [ops.pack_router_weights(torch.from_numpy(W.router_weights(cfg, l)).to(dev)) for l in range(nl)]
     logits = torch.empty((T, E), dtype=torch.float32, device=dev)
     ws = ops.select_workspace(T, E, k, dev)
     stats_all = torch.empty((nblocks, nl, L.NUM_STATS), dtype=torch.int32, device=dev)

@@ -82,17 +82,35 @@ extern "C" {
 #define ACCEPTMOE_MAX_TREE_NODES 1024
 
 /*
+ * acceptmoe_packed_router_bytes -- bytes of a packed router matrix:
+ *   ceil(E / 16) * 16 * H * 4 (0 for unsupported E or H).
+ * acceptmoe_pack_router_weights -- converts the fp32 router matrix W_r
+ * [E, H] (nn.Linear orientation, row-major) into the layout acceptmoe_route
+ * reads: rows padded with zeros to a multiple of 16, then for every 16-row
+ * tile and every 16-column chunk the 16 x 16 block is stored as 64 lanes x
+ * 16 B, lane L holding row (L % 16), columns 4*(L / 16) .. +3 of the chunk
+ * (the fp32 case of the expert-weight packing).  A one-time, load-time step.
+ *
+ *   src  [E, H] fp32 device;  dst device, acceptmoe_packed_router_bytes(E, H)
+ *   bytes, must not overlap src.  1 <= E <= ACCEPTMOE_MAX_EXPERTS,
+ *   H >= 16 and H % 16 == 0; both 16-byte aligned.
+ */
+size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H);
+int32_t acceptmoe_pack_router_weights(const float* src, int32_t E, int32_t H, float* dst, void* stream);
+
+/*
  * acceptmoe_route -- router logits z_t = W_r h_t for every node of the block
  * (Sec. 3.1, the target-router logits z_t the selector consumes).
  *
- *   hidden        [T, H] device, element type `hidden_dtype` (F32 or BF16)
- *   router_w      [E, H] device fp32 (nn.Linear orientation)
- *   logits        [T, E] device fp32, written
+ *   hidden         [T, H] device, element type `hidden_dtype` (F32 or BF16),
+ *                  16-byte aligned
+ *   router_packed  W_r [E, H] fp32 in the layout of acceptmoe_pack_router_weights
+ *   logits         [T, E] device fp32, written
  *   T >= 0 (T == 0 is a no-op), 1 <= E <= ACCEPTMOE_MAX_EXPERTS,
  *   H >= 16 and H % 16 == 0.
  * Accumulation is fp32; the result is deterministic (fixed reduction order).
  */
-int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const float* router_w,
+int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const float* router_packed,
                         int32_t T, int32_t H, int32_t E, float* logits, void* stream);
 
 /*

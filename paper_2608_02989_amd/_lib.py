@@ -36,6 +36,8 @@ _i32 = ctypes.c_int32
 _sz = ctypes.c_size_t
 
 SIGNATURES = {
+    "acceptmoe_packed_router_bytes": (ctypes.c_size_t, [_i32, _i32]),
+    "acceptmoe_pack_router_weights": (_i32, [_vp, _i32, _i32, _vp, _vp]),
     "acceptmoe_route": (_i32, [_vp, _i32, _vp, _i32, _i32, _i32, _vp, _vp]),
     "acceptmoe_select_workspace_size": (_sz, [_i32, _i32, _i32]),
     "acceptmoe_select": (_i32, [_vp, _vp, _vp, _vp, ctypes.POINTER(_i32), _i32, _i32, _i32, _i32,

@@ -40,7 +40,29 @@ const char* acceptmoe_last_error(void) { return g_err; }
 int32_t acceptmoe_version(void) { return 100; }
 
 // ---------------------------------------------------------------------------
-int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const float* router_w, int32_t T,
+size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H) {
+  if (E < 1 || E > ACCEPTMOE_MAX_EXPERTS || H < 16 || H % 16 != 0) return 0;
+  return amoe::packed_router_bytes(E, H);
+}
+
+int32_t acceptmoe_pack_router_weights(const float* src, int32_t E, int32_t H, float* dst, void* stream) {
+  clear_err();
+  if (E < 1 || E > ACCEPTMOE_MAX_EXPERTS)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "pack_router: E must be in [1, %d] (got %d)", ACCEPTMOE_MAX_EXPERTS, E);
+  if (H < 16 || H % 16 != 0)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "pack_router: H must be a positive multiple of 16 (got %d)", H);
+  if (!src || !dst) return fail(ACCEPTMOE_ERR_INVALID_ARG, "pack_router: null pointer");
+  if (!aligned(src, 16) || !aligned(dst, 16))
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "pack_router: src and dst must be 16-byte aligned");
+  const char* s = reinterpret_cast<const char*>(src);
+  const char* d = reinterpret_cast<const char*>(dst);
+  const size_t sbytes = static_cast<size_t>(E) * H * sizeof(float), dbytes = amoe::packed_router_bytes(E, H);
+  if (s < d + dbytes && d < s + sbytes) return fail(ACCEPTMOE_ERR_INVALID_ARG, "pack_router: src and dst overlap");
+  hipError_t e = amoe::launch_pack_router(src, E, H, dst, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "pack_router launch");
+}
+
+int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const float* router_packed, int32_t T,
                         int32_t H, int32_t E, float* logits, void* stream) {
   clear_err();
   if (T < 0) return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: T must be >= 0 (got %d)", T);
@@ -51,10 +73,10 @@ int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const float* r
   if (hidden_dtype != ACCEPTMOE_F32 && hidden_dtype != ACCEPTMOE_BF16)
     return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: unknown hidden dtype %d", hidden_dtype);
   if (T == 0) return ACCEPTMOE_OK;
-  if (!hidden || !router_w || !logits) return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: null pointer");
-  if (!aligned(hidden, 16) || !aligned(router_w, 16) || !aligned(logits, 4))
-    return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: hidden/router_w must be 16-byte aligned");
-  hipError_t e = amoe::launch_route(hidden, hidden_dtype == ACCEPTMOE_BF16, router_w, T, H, E, logits,
+  if (!hidden || !router_packed || !logits) return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: null pointer");
+  if (!aligned(hidden, 16) || !aligned(router_packed, 16) || !aligned(logits, 4))
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: hidden/router_packed must be 16-byte aligned");
+  hipError_t e = amoe::launch_route(hidden, hidden_dtype == ACCEPTMOE_BF16, router_packed, T, H, E, logits,
                                     static_cast<hipStream_t>(stream));
   return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "route launch");
 }

@@ -1,10 +1,15 @@
 // Router logits z_t = W_r h_t (Sec. 3.1): an fp32 [T,H] x [E,H]^T product on
 // the fp32 MFMA (v_mfma_f32_16x16x4f32), one 16-token x 16-expert tile per
-// workgroup of 16 waves.  Each wave reduces a contiguous slice of H; the
-// loads of a batch of 8 chunks are all issued before its first MFMA, so a
-// wave waits for memory once per batch rather than once per chunk (rows past
-// T / E are clamped, computed and dropped).  The 16 partial tiles are summed
-// in LDS in a fixed order (deterministic).
+// workgroup of 16 waves, each wave reducing a slice of H.
+//
+// Both operands are read with whole-cache-line accesses: the router weights
+// come pre-packed in MFMA fragment order (one contiguous 1 KiB read per
+// 16-expert x 16-column chunk, see acceptmoe_pack_router_weights), and the
+// workgroup's 16 hidden rows are staged in LDS with row-contiguous loads
+// before the waves read their A fragments from there.  A wave issues all of
+// its weight loads for a staged block before waiting for the staging, so the
+// two transfers overlap.  The 16 partial tiles are summed in LDS in a fixed
+// order (deterministic).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -13,70 +18,103 @@ namespace amoe {
 namespace {
 
 constexpr int kRouteWaves = 16;
-constexpr int kRouteBatch = 8;  // 16-wide K chunks loaded ahead of their MFMAs
+constexpr int kRouteThreads = kRouteWaves * kWave;
+constexpr int kRouteStageBytes = 64 * 1024;  // hidden bytes staged per block (16 rows)
+constexpr int kRouteBatch = 8;               // 16-wide K chunks per wave and staged block
+constexpr int kRouteRowPad = 16;             // bytes appended to each staged row (LDS banks)
 
-// Raw loads of four consecutive inputs, widened to fp32 only after the whole
-// batch has been issued (widening right after each load would make the wave
-// wait for it before issuing the next).
-__device__ __forceinline__ float4 load_raw(const float* p) { return *reinterpret_cast<const float4*>(p); }
-__device__ __forceinline__ uint2 load_raw(const uint16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+// Router weights packed like an fp32 expert stack with N = E rows padded to a
+// multiple of 16 with zeros: fragment (expert tile et, chunk c) holds, for
+// lane L = r + 16 g, the floats 4g .. 4g+3 of columns 16c .. 16c+15 of row
+// 16 et + r.
+__global__ void pack_router_kernel(const float4* __restrict__ src, float4* __restrict__ dst, int E, int H) {
+  const int nchunk = H / 16;
+  const size_t total = static_cast<size_t>((E + 15) / 16) * nchunk * kWave;
+  for (size_t q = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x; q < total;
+       q += static_cast<size_t>(gridDim.x) * blockDim.x) {
+    const int lane = static_cast<int>(q & 63);
+    const size_t f = q >> 6;
+    const int c = static_cast<int>(f % nchunk);
+    const int et = static_cast<int>(f / nchunk);
+    const int row = et * 16 + (lane & 15);
+    dst[q] = row < E ? src[(static_cast<size_t>(row) * H + c * 16 + 4 * (lane >> 4)) / 4]
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+}
 
-__device__ __forceinline__ float4 widen(const float4& v) { return v; }
-__device__ __forceinline__ float4 widen(const uint2& v) {
+__device__ __forceinline__ float4 widen4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 widen4(const uint16_t* p) {
+  const uint2 v = *reinterpret_cast<const uint2*>(p);
   return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
                      __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
 }
 
+// grid (ceil(E/16), ceil(T/16)), block 1024.  Lane (r, g) of a wave: token row
+// t0 + r of the A tile and expert 16 et + r of the B tile; component j of K
+// slice g of chunk c is column 16c + 4g + j (same for both operands).
 template <typename TIn>
-struct Raw4 {
-  typedef float4 type;
-};
-template <>
-struct Raw4<uint16_t> {
-  typedef uint2 type;
-};
-
-// grid (ceil(E/16), ceil(T/16)), block 1024.  Lane (r, g): token row t0 + r of
-// the A tile and expert column e0 + r of the B tile; K slice g of each
-// 16-wide chunk is the float4 at offset 4g, component j feeds MFMA j.
-template <typename TIn>
-__global__ __launch_bounds__(kRouteWaves * kWave) void route_kernel(const TIn* __restrict__ hidden,
-                                                                   const float* __restrict__ w, int T, int H,
-                                                                   int E, float* __restrict__ logits) {
+__global__ __launch_bounds__(kRouteThreads) void route_kernel(const TIn* __restrict__ hidden,
+                                                             const float4* __restrict__ wp, int T, int H, int E,
+                                                             float* __restrict__ logits) {
+  constexpr int kEb = sizeof(TIn);
+  constexpr int kBlockCols = kRouteStageBytes / (16 * kEb);  // staged columns per block
+  constexpr int kRowBytes = kBlockCols * kEb + kRouteRowPad;
+  static_assert(kBlockCols / 16 <= kRouteWaves * kRouteBatch, "a staged block must fit the wave batches");
+  __shared__ __align__(16) unsigned char hs[16 * kRowBytes];
   __shared__ floatx4 part[kRouteWaves][kWave];
+  const int tid = threadIdx.x;
   const int wave = wave_id();
   const int lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
-  const int e0 = blockIdx.x * 16, t0 = blockIdx.y * 16;
-  const int t = min(t0 + r, T - 1), e = min(e0 + r, E - 1);
-  const TIn* hrow = hidden + static_cast<size_t>(t) * H + 4 * g;
-  const float* wrow = w + static_cast<size_t>(e) * H + 4 * g;
-
-  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  const int et = blockIdx.x, t0 = blockIdx.y * 16;
   const int nchunk = H / 16;
-  const int c0 = wave * nchunk / kRouteWaves, c1 = (wave + 1) * nchunk / kRouteWaves;
-  for (int cb = c0; cb < c1; cb += kRouteBatch) {
-    // chunks past c1 re-read chunk c1 - 1 and are not used
-    typename Raw4<TIn>::type ar[kRouteBatch];
+  const float4* wrow = wp + static_cast<size_t>(et) * nchunk * kWave + lane;
+
+  floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  for (int kb0 = 0; kb0 < H; kb0 += kBlockCols) {
+    const int cols = min(kBlockCols, H - kb0);
+    const int nc = cols / 16;
+    // this wave's chunks of the block: [c0, c1), at most kRouteBatch of them
+    const int c0 = wave * nc / kRouteWaves, c1 = (wave + 1) * nc / kRouteWaves;
+    const int clast = max(c1 - 1, c0);  // in range whenever the wave has chunks
     float4 b[kRouteBatch];
 #pragma unroll
     for (int i = 0; i < kRouteBatch; ++i) {
-      const int c = min(cb + i, c1 - 1);
-      ar[i] = load_raw(hrow + c * 16);
-      b[i] = load_raw(wrow + c * 16);
+      const int c = kb0 / 16 + min(min(c0 + i, clast), nc - 1);  // chunks past c1 re-read one and go unused
+      b[i] = wrow[static_cast<size_t>(c) * kWave];
     }
-    // keep the scheduler from sinking each load down to its MFMA
-    __builtin_amdgcn_sched_barrier(0);
+    // stage rows t0 .. t0+15 (clamped to T-1; those rows are computed and dropped)
+    const int pieces_per_row = cols * kEb / 16;
+    if (kb0 > 0) __syncthreads();  // the previous block's fragments are consumed
+    for (int i = tid; i < 16 * pieces_per_row; i += kRouteThreads) {
+      const int row = i / pieces_per_row, q = i % pieces_per_row;
+      const int t = min(t0 + row, T - 1);
+      const uint4 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const unsigned char*>(hidden) +
+                                                      (static_cast<size_t>(t) * H + kb0) * kEb + q * 16);
+      *reinterpret_cast<uint4*>(hs + row * kRowBytes + q * 16) = v;
+    }
+    __syncthreads();
+    const unsigned char* arow = hs + r * kRowBytes + 4 * g * kEb;
 #pragma unroll
-    for (int i = 0; i < kRouteBatch; ++i) {
-      const float4 a = widen(ar[i]);
-      floatx4 n = mfma_f32_16x16x4(a.x, b[i].x, acc);
-      n = mfma_f32_16x16x4(a.y, b[i].y, n);
-      n = mfma_f32_16x16x4(a.z, b[i].z, n);
-      n = mfma_f32_16x16x4(a.w, b[i].w, n);
-      acc = cb + i < c1 ? n : acc;  // wave-uniform select, no branch
+    for (int i = 0; i < kRouteBatch; i += 2) {
+      const int ca = min(min(c0 + i, clast), nc - 1), cb = min(min(c0 + i + 1, clast), nc - 1);
+      const float4 a0 = widen4(reinterpret_cast<const TIn*>(arow + ca * 16 * kEb));
+      const float4 a1 = widen4(reinterpret_cast<const TIn*>(arow + cb * 16 * kEb));
+      floatx4 n0 = mfma_f32_16x16x4(a0.x, b[i].x, acc0);
+      floatx4 n1 = mfma_f32_16x16x4(a1.x, b[i + 1].x, acc1);
+      n0 = mfma_f32_16x16x4(a0.y, b[i].y, n0);
+      n1 = mfma_f32_16x16x4(a1.y, b[i + 1].y, n1);
+      n0 = mfma_f32_16x16x4(a0.z, b[i].z, n0);
+      n1 = mfma_f32_16x16x4(a1.z, b[i + 1].z, n1);
+      n0 = mfma_f32_16x16x4(a0.w, b[i].w, n0);
+      n1 = mfma_f32_16x16x4(a1.w, b[i + 1].w, n1);
+      acc0 = c0 + i < c1 ? n0 : acc0;  // wave-uniform selects, no branch
+      acc1 = c0 + i + 1 < c1 ? n1 : acc1;
     }
   }
+  floatx4 acc;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = acc0[i] + acc1[i];
   part[wave][lane] = acc;
   __syncthreads();
   if (wave == 0) {
@@ -89,11 +127,12 @@ __global__ __launch_bounds__(kRouteWaves * kWave) void route_kernel(const TIn* _
       s[2] += q[2];
       s[3] += q[3];
     }
-    if (e0 + r < E) {
+    const int e = et * 16 + r;
+    if (e < E) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int tt = t0 + 4 * g + i;
-        if (tt < T) logits[static_cast<size_t>(tt) * E + e0 + r] = s[i];
+        if (tt < T) logits[static_cast<size_t>(tt) * E + e] = s[i];
       }
     }
   }
@@ -101,16 +140,27 @@ __global__ __launch_bounds__(kRouteWaves * kWave) void route_kernel(const TIn* _
 
 }  // namespace
 
-hipError_t launch_route(const void* hidden, int hidden_is_bf16, const float* router_w, int T, int H,
-                        int E, float* logits, hipStream_t stream) {
+size_t packed_router_bytes(int E, int H) { return static_cast<size_t>((E + 15) / 16) * 16 * H * sizeof(float); }
+
+hipError_t launch_pack_router(const float* src, int E, int H, float* dst, hipStream_t stream) {
+  const size_t pieces = packed_router_bytes(E, H) / 16;
+  const int block = 256;
+  const size_t want = (pieces + block - 1) / block;
+  const int grid = static_cast<int>(want < 65536 ? want : 65536);
+  pack_router_kernel<<<grid, block, 0, stream>>>(reinterpret_cast<const float4*>(src), reinterpret_cast<float4*>(dst),
+                                                 E, H);
+  return hipGetLastError();
+}
+
+hipError_t launch_route(const void* hidden, int hidden_is_bf16, const float* router_packed, int T, int H, int E,
+                        float* logits, hipStream_t stream) {
   dim3 grid((E + 15) / 16, (T + 15) / 16);
-  const int block = kRouteWaves * kWave;
+  const float4* wp = reinterpret_cast<const float4*>(router_packed);
   if (hidden_is_bf16)
-    route_kernel<uint16_t><<<grid, block, 0, stream>>>(static_cast<const uint16_t*>(hidden), router_w, T, H,
-                                                       E, logits);
+    route_kernel<uint16_t><<<grid, kRouteThreads, 0, stream>>>(static_cast<const uint16_t*>(hidden), wp, T, H, E,
+                                                                logits);
   else
-    route_kernel<float><<<grid, block, 0, stream>>>(static_cast<const float*>(hidden), router_w, T, H, E,
-                                                    logits);
+    route_kernel<float><<<grid, kRouteThreads, 0, stream>>>(static_cast<const float*>(hidden), wp, T, H, E, logits);
   return hipGetLastError();
 }
 

@@ -56,6 +56,7 @@ struct SelShared {
   alignas(16) uint8_t inSp[kMaxExperts];
   alignas(16) uint8_t routed[kMaxExperts];
   alignas(16) uint8_t resident[kMaxExperts];
+  alignas(16) int rpart[kSelThreads];  // partial rank counts
 };
 
 // per-wave compaction scratch for top-k slot ordering
@@ -133,17 +134,19 @@ __device__ __forceinline__ int slot_of(int j, int n, const uint32_t* sk, const i
   return r;
 }
 
-// rank[e] for every flagged e (entries of unflagged experts are left at 0):
-// the E x E comparison is split over all threads of the workgroup, each thread
-// counting one slice of competitors for one expert; integer partial counts
-// are added with LDS atomics (order-independent).  rank must be zeroed first.
+// rank[e] for every flagged e (0 for unflagged experts): the E x E comparison
+// is split over all threads of the workgroup, thread (part, e) counting the
+// flagged competitors of e in one slice of the index range (threads of a wave
+// share the slice, so their LDS reads are broadcasts); the partial counts are
+// stored and added per expert after a barrier.  The caller synchronizes
+// before reading rank.
 template <bool kDesc>
-__device__ __forceinline__ void rank_all(const double* v, const uint8_t* flag, int E, int* rank, int tid) {
+__device__ __forceinline__ void rank_all(const double* v, const uint8_t* flag, int E, int* rank, int* part_cnt,
+                                         int tid) {
   const int parts = E <= 128 ? 8 : (E <= 256 ? 4 : 2);
   const int span = ((E + parts - 1) / parts + 7) & ~7;  // competitors per slice, multiple of 8
   for (int item = tid; item < E * parts; item += kSelThreads) {
-    const int e = item / parts, part = item % parts;
-    if (!flag[e]) continue;
+    const int part = item / E, e = item % E;
     const double ve = v[e];
     const int j_begin = part * span;
     const int j_end = min(E, j_begin + span);
@@ -162,7 +165,13 @@ __device__ __forceinline__ void rank_all(const double* v, const uint8_t* flag, i
         r += static_cast<int>(fl & (beats | ((vv[q] == ve) & (j0 + q < e))));
       }
     }
-    if (r) atomicAdd(&rank[e], r);
+    part_cnt[item] = flag[e] ? r : 0;
+  }
+  __syncthreads();
+  if (tid < E) {
+    int r = 0;
+    for (int q = 0; q < parts; ++q) r += part_cnt[q * E + tid];
+    rank[tid] = r;
   }
 }
 
@@ -319,6 +328,16 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
     sh.resident[e] = (e < E) ? (has_mask ? (p.resident[e] != 0) : 1) : 0;
   }
   if (tid < kRoutedWords) p.ws_routed[b * kRoutedWords + tid] = 0u;
+  // the first utility chunk's natural top-k entries, loaded now so their
+  // latency overlaps the node loads below
+  const int chunk = kDenseDoubles / E;  // >= 8 for E <= 512
+  int pf_e = 0;
+  double pf_r = 0.0;
+  if (tid < min(chunk, Tb) * k) {
+    const size_t gi = static_cast<size_t>(t_begin) * k + tid;
+    pf_e = p.ws_kidx[gi];
+    pf_r = p.ws_r[gi];
+  }
   int my_d = -1;
   float my_p = 0.0f;
   if (tid < Tb) {
@@ -364,7 +383,6 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
 
   // ---------------- P3: votes, anchor, utility in node order ----------------
   double u_acc = 0.0;
-  const int chunk = kDenseDoubles / E;  // >= 8 for E <= 512
   for (int c0 = 0; c0 < Tb; c0 += chunk) {
     const int cn = min(chunk, Tb - c0);
     for (int i = tid; i < cn * E; i += kSelThreads) sh.dense[i] = 0.0;
@@ -372,8 +390,9 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
     for (int i = tid; i < cn * k; i += kSelThreads) {
       const int tl = c0 + i / k;
       const size_t gi = static_cast<size_t>(t_begin + tl) * k + (i % k);
-      const int e = p.ws_kidx[gi];
-      sh.dense[(tl - c0) * E + e] = sh.alpha[tl] * p.ws_r[gi];
+      const bool pf = c0 == 0 && i == tid;  // loaded at the start
+      const int e = pf ? pf_e : p.ws_kidx[gi];
+      sh.dense[(tl - c0) * E + e] = sh.alpha[tl] * (pf ? pf_r : p.ws_r[gi]);
       atomicAdd(&sh.votes[e], 1);
       if (tl == 0) sh.anchor[e] = 1;  // the root is the tree's only depth-0 node
     }
@@ -462,13 +481,13 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
 
   if (mode == MODE_SELF || mode == MODE_FIXED) {
     // S = A u first n_take of R in (u desc, index asc) order
-    rank_all<true>(sh.u, sh.inR, E, sh.rankv, tid);
+    rank_all<true>(sh.u, sh.inR, E, sh.rankv, sh.rpart, tid);
     __syncthreads();
     if (tid < E) sh.inS[tid] = sh.anchor[tid] || sh.rankv[tid] < sh.n_take;
   } else if (mode == MODE_ALL) {
     if (tid < E) sh.inS[tid] = 1;
   } else {
-    rank_all<true>(sh.score, sh.inC, E, sh.rankv, tid);
+    rank_all<true>(sh.score, sh.inC, E, sh.rankv, sh.rpart, tid);
     __syncthreads();
     if (tid < E) sh.inS[tid] = sh.rankv[tid] < bud;
   }
@@ -499,7 +518,7 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
       wg_count(c, &sh.n_C, lane);
     }
     __syncthreads();
-    rank_all<false>(sh.u, sh.inC, E, sh.rankv, tid);
+    rank_all<false>(sh.u, sh.inC, E, sh.rankv, sh.rpart, tid);
     __syncthreads();
     if (tid < E) {
       if (sh.inC[tid]) sh.pv[sh.rankv[tid]] = sh.votes[tid];

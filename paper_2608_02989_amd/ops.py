@@ -46,18 +46,37 @@ def _need(t: torch.Tensor, name: str, dtype=None, dim=None):
 
 
 # ---------------------------------------------------------------------------
-def route(hidden: torch.Tensor, router_w: torch.Tensor, out: torch.Tensor | None = None,
-          stream=None) -> torch.Tensor:
-    """Router logits [T, E] fp32 (acceptmoe_route)."""
-    _need(hidden, "hidden", dim=2)
+class PackedRouter:
+    """Router matrix W_r [E, H] fp32 in the layout acceptmoe_route reads."""
+
+    def __init__(self, data: torch.Tensor, E: int, H: int):
+        self.data, self.E, self.H = data, E, H
+
+
+def pack_router_weights(router_w: torch.Tensor, stream=None) -> PackedRouter:
+    """[E, H] fp32 router matrix -> PackedRouter (acceptmoe_pack_router_weights)."""
     _need(router_w, "router_w", torch.float32, 2)
+    E, H = router_w.shape
+    n = int(lib().acceptmoe_packed_router_bytes(E, H))
+    if n == 0:
+        raise ValueError(f"unsupported router shape {tuple(router_w.shape)}")
+    data = torch.empty(n // 4, dtype=torch.float32, device=router_w.device)
+    check(lib().acceptmoe_pack_router_weights(_ptr(router_w), E, H, _ptr(data), _stream_ptr(stream)))
+    return PackedRouter(data, E, H)
+
+
+def route(hidden: torch.Tensor, router: PackedRouter, out: torch.Tensor | None = None,
+          stream=None) -> torch.Tensor:
+    """Router logits [T, E] fp32 (acceptmoe_route) from a packed router matrix."""
+    _need(hidden, "hidden", dim=2)
+    if not isinstance(router, PackedRouter):
+        raise TypeError("route needs the router matrix packed by pack_router_weights")
     T, H = hidden.shape
-    E = router_w.shape[0]
-    if router_w.shape[1] != H:
-        raise ValueError("router_w must be [E, H]")
+    if router.H != H:
+        raise ValueError(f"router packed for H={router.H}, hidden has H={H}")
     if out is None:
-        out = torch.empty((T, E), dtype=torch.float32, device=hidden.device)
-    check(lib().acceptmoe_route(_ptr(hidden), _dtype_code(hidden), _ptr(router_w), T, H, E, _ptr(out),
+        out = torch.empty((T, router.E), dtype=torch.float32, device=hidden.device)
+    check(lib().acceptmoe_route(_ptr(hidden), _dtype_code(hidden), _ptr(router.data), T, H, router.E, _ptr(out),
                                 _stream_ptr(stream)))
     return out
 
@@ -162,7 +181,8 @@ class VerifyLayer:
                  w_down: torch.Tensor, k: int, max_tokens: int, max_trees: int = 1, beta: float = 0.5,
                  mode: int = L.MODE_SELF_SIZING, budget: int = 0, removal_cap: int = -1,
                  packed: bool = False):
-        self.router_w = router_w
+        self.router_w = router_w  # [E, H] fp32, kept for reference checks
+        self.router = pack_router_weights(router_w)
         self.E, self.I, self.H = w_gate.shape
         self.k, self.beta, self.mode, self.budget, self.removal_cap = k, beta, mode, budget, removal_cap
         self.dtype = w_gate.dtype
@@ -189,7 +209,7 @@ class VerifyLayer:
         T = hidden.shape[0]
         B = 1 if tree_offsets is None else len(tree_offsets) - 1
         logits = self.logits[:T]
-        route(hidden, self.router_w, out=logits, stream=stream)
+        route(hidden, self.router, out=logits, stream=stream)
         outs = {"eligible": self.sel_out["eligible"][:B], "idx": self.sel_out["idx"][:T],
                 "gate": self.sel_out["gate"][:T], "stats": self.sel_out["stats"][:B]}
         select(logits, parent, depth, prob, tree_offsets, self.k, self.beta, self.mode, self.budget,

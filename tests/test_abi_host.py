@@ -58,6 +58,21 @@ def status_and_msg(rc):
     return rc, L.lib().acceptmoe_last_error().decode()
 
 
+def test_pack_router_sizes_and_rejects():
+    lib = L.lib()
+    assert lib.acceptmoe_packed_router_bytes(128, 2048) == 128 * 2048 * 4
+    assert lib.acceptmoe_packed_router_bytes(37, 256) == 48 * 256 * 4     # rows padded to 16
+    assert lib.acceptmoe_packed_router_bytes(0, 256) == 0
+    assert lib.acceptmoe_packed_router_bytes(16, 250) == 0
+    f = lib.acceptmoe_pack_router_weights
+    assert f(FAKE, 0, 256, FAKE, None) == L.ERR_UNSUPPORTED
+    assert f(FAKE, 16, 250, FAKE, None) == L.ERR_UNSUPPORTED
+    assert f(None, 16, 256, FAKE, None) == L.ERR_INVALID_ARG
+    assert f(V(0x100004), 16, 256, FAKE, None) == L.ERR_INVALID_ARG       # misaligned
+    rc, msg = status_and_msg(f(V(0x100000), 16, 256, V(0x100000 + 256), None))
+    assert rc == L.ERR_INVALID_ARG and "overlap" in msg
+
+
 def test_route_rejects():
     f = L.lib().acceptmoe_route
     assert status_and_msg(f(FAKE, L.BF16, FAKE, -1, 256, 16, FAKE, None))[0] == L.ERR_INVALID_ARG

@@ -64,12 +64,13 @@ def test_route_parity(gpu, name, T, E):
     hdev, h64 = hidden_for(cfg, blk.hidden)
     rw = W.router_weights(cfg)
     say(f"route {name} T={len(h64)} E={cfg.E} H={cfg.H}")
-    z = ops.route(to_dev_hidden(cfg, hdev), f32(rw)).cpu().numpy()
+    rp = ops.pack_router_weights(f32(rw))
+    z = ops.route(to_dev_hidden(cfg, hdev), rp).cpu().numpy()
     ref = O.route(h64, rw.astype(np.float64))
     err = normwise_rel(z, ref)
     assert err <= LOGIT_TOL, err
     # fixed reduction order: identical on a second call
-    z2 = ops.route(to_dev_hidden(cfg, hdev), f32(rw)).cpu().numpy()
+    z2 = ops.route(to_dev_hidden(cfg, hdev), rp).cpu().numpy()
     assert np.array_equal(z.view(np.uint32), z2.view(np.uint32))
 
 
@@ -289,6 +290,24 @@ def test_forward_parity_ragged_and_hot_expert(gpu, dtype, T):
     err = normwise_rel(got, ref)
     assert err <= FWD_TOL[cfg.dtype], err
     assert np.all(got[6] == 0.0)
+
+
+def test_pack_router_layout_documented(gpu):
+    # values encode (e, h); rows past E are zero
+    E, H = 20, 48
+    e_, h_ = np.meshgrid(np.arange(E), np.arange(H), indexing="ij")
+    src = (e_ * 1000 + h_ + 1).astype(np.float32)
+    rp = ops.pack_router_weights(f32(src))
+    packed = rp.data.cpu().numpy().reshape(-1, 64, 4)     # [fragment][lane][4 floats]
+    nchunk = H // 16
+    assert packed.shape[0] == ((E + 15) // 16) * nchunk
+    for f in range(packed.shape[0]):
+        et, c = divmod(f, nchunk)
+        for lane in range(64):
+            row = et * 16 + lane % 16
+            cols = c * 16 + 4 * (lane // 16) + np.arange(4)
+            want = src[row, cols] if row < E else np.zeros(4, np.float32)
+            assert np.array_equal(packed[f, lane], want), (f, lane)
 
 
 def test_pack_layout_documented(gpu):
