@@ -204,7 +204,8 @@ size_t acceptmoe_moe_forward_workspace_size(int32_t T, int32_t H, int32_t I, int
  *                 expert repeated within a row is used once (at its first slot)
  *   topk_gate     [T, k] fp32 device
  *   out           [T, H] fp32 device, written (every element)
- *   workspace     acceptmoe_moe_forward_workspace_size(...) bytes
+ *   workspace     acceptmoe_moe_forward_workspace_size(...) bytes, 256-byte
+ *                 aligned, not shared by calls that may run concurrently
  *   Limits: H % 32 == 0 and I % 32 == 0 (bf16), H % 16 == 0 and I % 16 == 0
  *   (fp32); 1 <= E <= ACCEPTMOE_MAX_EXPERTS; 1 <= k <= ACCEPTMOE_MAX_TOPK;
  *   T == 0 is a no-op.

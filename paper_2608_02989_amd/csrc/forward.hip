@@ -667,10 +667,12 @@ struct SelfDispatchSlot<false> {
 // Work item i = (active expert i / wg_per_expert, tile run i % wg_per_expert).
 // Without kSelf: grid.x = cap_experts * wg_per_expert, one item per
 // workgroup, reading dispatch_kernel's CSR.  kSelf (gate/up pass, blocks of up
-// to kSelfMaxT tokens): a grid of at most kSelfGrid workgroups (about three
-// per CU, all resident) builds the dispatch in LDS once and takes items
-// blockIdx.x, blockIdx.x + gridDim.x, ...
-constexpr int kSelfGrid = 768;
+// to kSelfMaxT tokens): a grid no larger than what is resident at once (so no
+// workgroup waits for a slot and repeats the dispatch) builds the dispatch in
+// LDS once per workgroup and takes items blockIdx.x, blockIdx.x + gridDim.x,
+// ...  (A device-wide work counter was tried: every workgroup's first atomic
+// hits the same address at once and the serialized atomics cost more than
+// the balance gained.)
 
 template <class P, Proj F, int MTMAX, int NTW, int KS, bool kSelf, int KMAX>
 __global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
@@ -716,59 +718,65 @@ __global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
 
 // ---------------------------------------------------------------------------
 // Column-tile down pass (blocks of up to kColMaxT tokens).  A workgroup owns
-// one 16-column tile of H and one of `ksplit` (1 or 2) parts of I.  It
-// streams that tile's rows of W_d for every down item (expert e, 16-token
+// NB adjacent 16-column tiles of H and one of `ksplit` (1 or 2) parts of I.
+// It streams those tiles' rows of W_d for every down item (expert e, 16-token
 // block of e's list): the items are dealt round-robin to the waves, and each
 // wave runs one continuous two-stage load pipeline across its items.  After
 // an item's last stage the wave adds gate * (act_e W_d^T) into its own LDS
-// accumulator out_w[t, 16 columns] (a token appears once per expert, so the
+// accumulator out_w[t, 16 NB columns] (a token appears once per expert, so the
 // lanes of one item never collide).  At the end the waves' accumulators are
 // summed in wave order and written to out, or added into the zeroed out when
 // I is split in two (two fp32 additions onto zero commute, so the result
 // does not depend on which half lands first).  Every workgroup does the same
-// work; its LDS footprint keeps it alone on its CU.
+// work; its LDS footprint keeps it alone on its CU.  Each workgroup reads
+// every dispatched activation row once, so NB = 2 halves that traffic per
+// column for wide H.
 // ---------------------------------------------------------------------------
-constexpr int kColWaves = 8;
+constexpr int kColLanes = 8;  // waves x NB: the accumulators take kColLanes x kColMaxT x 16 floats
 constexpr int kColMaxT = 256;
 constexpr int kColMaxSlots = 2048;
 constexpr int kColMaxItems = kMaxExperts + kColMaxSlots / 16;
 
 struct ColShared {
-  float acc[kColWaves][kColMaxT * 16];  // per-wave token accumulators
-  int tok[kColMaxSlots];                // CSR row -> token
-  float gw[kColMaxSlots];               // CSR row -> gate of that slot
+  float acc[kColLanes * kColMaxT * 16];  // per-wave token accumulators [wave][t][16 NB]
+  int tok[kColMaxSlots];                 // CSR row -> token
+  float gw[kColMaxSlots];                // CSR row -> gate of that slot
   int4 items[kColMaxItems];
 };
 
-template <class P, int kU>
-__global__ __launch_bounds__(kColWaves * kWave) void down_col_kernel(ForwardParams p, int ksplit) {
+template <class P, int kU, int NB>
+__global__ __launch_bounds__(kColLanes / NB * kWave) void down_col_kernel(ForwardParams p, int ksplit) {
+  constexpr int kWaves = kColLanes / NB;
+  constexpr int kThreads = kWaves * kWave;
+  constexpr int kCols = 16 * NB;
   __shared__ ColShared sh;
   const int tid = threadIdx.x;
   const int wave = wave_id(), lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
   const int T = p.T, H = p.H, k = p.k;
   const int ntiles = H / 16;
-  const int ht = blockIdx.x % ntiles, part = blockIdx.x / ntiles;
+  const int ngroups = ntiles / NB;
+  const int ht0 = (blockIdx.x % ngroups) * NB, part = blockIdx.x / ngroups;
   const int KC = p.I / P::kKF;
   const int kc0 = part * KC / ksplit;
   const int L = (KC / ksplit) / kU;  // pipeline stages per item
   const int rowq = p.I * P::kElemBytes / 16;
   const int n_items = *p.n_items;
   const int n_rows = p.off[p.E];
-  for (int i = tid; i < kColWaves * T * 16; i += kColWaves * kWave) sh.acc[i / (T * 16)][i % (T * 16)] = 0.f;
-  for (int i = tid; i < n_rows; i += kColWaves * kWave) {
+  for (int i = tid; i < kWaves * T * kCols; i += kThreads) sh.acc[i] = 0.f;
+  for (int i = tid; i < n_rows; i += kThreads) {
     const int slot = p.ent_slot[i];
     sh.tok[i] = slot / k;
     sh.gw[i] = p.topk_gate[slot];
   }
-  for (int i = tid; i < n_items; i += kColWaves * kWave) sh.items[i] = p.items[i];
+  for (int i = tid; i < n_items; i += kThreads) sh.items[i] = p.items[i];
   __syncthreads();
 
   const uint4* wd = static_cast<const uint4*>(p.w_down);
   const uint4* act = static_cast<const uint4*>(p.act);
-  float* accw = sh.acc[wave];
-  // items wave, wave + W, ...; stage = (item, q), q in [0, L)
-  const int my_items = n_items > wave ? (n_items - wave + kColWaves - 1) / kColWaves : 0;
+  float* accw = sh.acc + wave * T * kCols;
+  // items wave, wave + kWaves, ...; stage = (item, q), q in [0, L)
+  const int my_items = n_items > wave ? (n_items - wave + kWaves - 1) / kWaves : 0;
   const int nst = my_items * L;
   struct Cursor {
     int it, q, e, row0, nrows;
@@ -784,36 +792,45 @@ __global__ __launch_bounds__(kColWaves * kWave) void down_col_kernel(ForwardPara
   auto advance = [&](Cursor& c) {
     if (++c.q == L) {
       c.q = 0;
-      c.it += kColWaves;
+      c.it += kWaves;
       fetch(c);
     }
   };
-  uint4 w0[kU], x0[kU], w1[kU], x1[kU];
-  auto load = [&](uint4 (&wv)[kU], uint4 (&xv)[kU], const Cursor& c) {
+  uint4 w0[kU][NB], x0[kU], w1[kU][NB], x1[kU];
+  auto load = [&](uint4 (&wv)[kU][NB], uint4 (&xv)[kU], const Cursor& c) {
     const int kc = kc0 + c.q * kU;
-    const uint4* wp = wd + ((static_cast<size_t>(c.e) * ntiles + ht) * KC + kc) * kWave + lane;
     const uint4* xp = act + static_cast<size_t>(c.row0 + min(r, c.nrows - 1)) * rowq + g + kc * 4;
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
-      wv[u] = load_weight(wp + u * kWave);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        wv[u][nb] = load_weight(wd + ((static_cast<size_t>(c.e) * ntiles + ht0 + nb) * KC + kc + u) * kWave + lane);
       xv[u] = xp[u * 4];
     }
   };
-  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](uint4 (&wv)[kU], uint4 (&xv)[kU], Cursor& c) {
+  floatx4 acc[NB];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) acc = P::mma(xv[u], wv[u], acc);
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](uint4 (&wv)[kU][NB], uint4 (&xv)[kU], Cursor& c) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = P::mma(xv[u], wv[u][nb], acc[nb]);
     if (c.q == L - 1) {
-      // item done: out_w[t] += gate * row, rows 4g..4g+3 of the block, column r
+      // item done: out_w[t] += gate * row, rows 4g..4g+3 of the block, column r of each tile
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int m = 4 * g + i;
         if (m < c.nrows) {
           const int row = c.row0 + m;
-          accw[sh.tok[row] * 16 + r] += sh.gw[row] * acc[i];
+          float* dst = accw + sh.tok[row] * kCols + r;
+          const float gt = sh.gw[row];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) dst[16 * nb] += gt * acc[nb][i];
         }
       }
-      acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
     advance(c);
   };
@@ -842,11 +859,11 @@ __global__ __launch_bounds__(kColWaves * kWave) void down_col_kernel(ForwardPara
   }
   __syncthreads();
   // fixed-order sum over the waves, then out (or out += for a half of I)
-  for (int i = tid; i < T * 16; i += kColWaves * kWave) {
-    float v = sh.acc[0][i];
+  for (int i = tid; i < T * kCols; i += kThreads) {
+    float v = sh.acc[i];
 #pragma unroll
-    for (int w = 1; w < kColWaves; ++w) v += sh.acc[w][i];
-    float* o = p.out + static_cast<size_t>(i >> 4) * H + ht * 16 + (i & 15);
+    for (int w = 1; w < kWaves; ++w) v += sh.acc[w * T * kCols + i];
+    float* o = p.out + static_cast<size_t>(i / kCols) * H + ht0 * 16 + (i % kCols);
     if (ksplit == 2) atomicAdd(o, v);
     else *o = v;
   }
@@ -884,17 +901,38 @@ __global__ __launch_bounds__(256) void combine_kernel(ForwardParams p) {
   reinterpret_cast<float4*>(p.out + static_cast<size_t>(t) * H)[h4] = s;
 }
 
+// Workgroups of `kernel` (256 threads) resident on the current device at
+// once, computed on first use per device.
+template <class F>
+int resident_workgroups(F kernel) {
+  constexpr int kMaxDevices = 64;
+  static int cached[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = 0;
+  if (cached[dev] == 0) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess || per_cu < 1) per_cu = 1;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 1;
+    cached[dev] = per_cu * cus;
+  }
+  return cached[dev];
+}
+
 template <class P, int MTMAX>
 hipError_t launch_gate_up(const ForwardParams& p, int cap, bool self, hipStream_t stream) {
   constexpr int gt = ProjShape<Proj::GateUp, AMOE_GU_NTW, AMOE_GU_KS>::kTilesPerWG;
   const int items = cap * ((p.I / 16 + gt - 1) / gt);
-  const dim3 grid(self ? (items < kSelfGrid ? items : kSelfGrid) : items);
-  if (!self)
-    ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, false, 8><<<grid, 256, 0, stream>>>(p);
-  else if (p.k <= 8)
-    ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, 8><<<grid, 256, 0, stream>>>(p);
-  else
-    ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, kMaxTopK><<<grid, 256, 0, stream>>>(p);
+  if (!self) {
+    ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, false, 8><<<dim3(items), 256, 0, stream>>>(p);
+  } else if (p.k <= 8) {
+    auto kern = ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, 8>;
+    const int res = resident_workgroups(kern);
+    kern<<<dim3(items < res ? items : res), 256, 0, stream>>>(p);
+  } else {
+    auto kern = ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, kMaxTopK>;
+    const int res = resident_workgroups(kern);
+    kern<<<dim3(items < res ? items : res), 256, 0, stream>>>(p);
+  }
   return hipGetLastError();
 }
 
@@ -906,17 +944,19 @@ hipError_t launch_down_rows(const ForwardParams& p, int cap, hipStream_t stream)
   return hipGetLastError();
 }
 
-// Column-tile down pass shape: I split in two when H has at most 128 column
-// tiles (so about 256 workgroups run), k-steps per pipeline stage dividing
-// the part of I.
+// Column-tile down pass shape: I split in two when that keeps the grid near
+// 256 workgroups, two column tiles per workgroup for wide H, k-steps per
+// pipeline stage dividing the part of I.
 struct ColShape {
-  int ksplit, ku;
+  int ksplit, ku, nb;
 };
 
 ColShape col_shape(int H, int I, int is_bf16) {
   const int KC = I / (is_bf16 ? Bf16Path::kKF : F32Path::kKF);
+  const int ntiles = H / 16;
   ColShape c;
-  c.ksplit = (H / 16 <= 128 && KC % 2 == 0) ? 2 : 1;
+  c.nb = (ntiles >= 256 && ntiles % 2 == 0) ? 2 : 1;
+  c.ksplit = (ntiles / c.nb <= 128 && KC % 2 == 0) ? 2 : 1;
   const int len = KC / c.ksplit;
   c.ku = len % 4 == 0 ? 4 : (len % 2 == 0 ? 2 : 1);
   return c;
@@ -929,13 +969,19 @@ bool use_col_path(int T, int k) {
          static_cast<long long>(T) * k <= kSelfMaxSlots;
 }
 
+template <class P, int NB>
+hipError_t launch_down_col_nb(const ForwardParams& p, const ColShape& c, hipStream_t stream) {
+  const dim3 grid((p.H / 16 / NB) * c.ksplit);
+  constexpr int threads = kColLanes / NB * kWave;
+  if (c.ku == 4) down_col_kernel<P, 4, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+  else if (c.ku == 2) down_col_kernel<P, 2, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+  else down_col_kernel<P, 1, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+  return hipGetLastError();
+}
+
 template <class P>
 hipError_t launch_down_col(const ForwardParams& p, const ColShape& c, hipStream_t stream) {
-  const dim3 grid((p.H / 16) * c.ksplit);
-  if (c.ku == 4) down_col_kernel<P, 4><<<grid, kColWaves * kWave, 0, stream>>>(p, c.ksplit);
-  else if (c.ku == 2) down_col_kernel<P, 2><<<grid, kColWaves * kWave, 0, stream>>>(p, c.ksplit);
-  else down_col_kernel<P, 1><<<grid, kColWaves * kWave, 0, stream>>>(p, c.ksplit);
-  return hipGetLastError();
+  return c.nb == 2 ? launch_down_col_nb<P, 2>(p, c, stream) : launch_down_col_nb<P, 1>(p, c, stream);
 }
 
 }  // namespace
