@@ -125,6 +125,23 @@ __device__ __forceinline__ int wave_sum_i32(int v) {
   return static_cast<int>(dpp::reduce(static_cast<uint32_t>(v), 0u, [](uint32_t a, uint32_t b) { return a + b; }));
 }
 
+// Inclusive prefix sum over the 64 lanes on DPP moves: Hillis-Steele within
+// each row of 16 (shifts 1, 2, 4, 8; lanes without a source add 0), then row
+// 15's total into rows 1 and 3 and lane 31's into rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan_i32(int v) {
+  const uint32_t z = 0u;
+  uint32_t x = static_cast<uint32_t>(v);
+  x += dpp::mov<0x111>(z, x);  // row_shr:1
+  x += dpp::mov<0x112>(z, x);  // row_shr:2
+  x += dpp::mov<0x114>(z, x);  // row_shr:4
+  x += dpp::mov<0x118>(z, x);  // row_shr:8
+  x += dpp::mov<dpp::kBcast15, 0xA>(z, x);
+  x += dpp::mov<dpp::kBcast31, 0xC>(z, x);
+  return static_cast<int>(x);
+}
+
+__device__ __forceinline__ int lane_value(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
+
 // Orders LDS traffic between the lanes of one wave (no cross-wave barrier).
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");

@@ -77,11 +77,7 @@ __device__ __forceinline__ int scan_experts(const int* cnt, int* off, int* activ
   for (int e0 = 0; e0 < E; e0 += kWave) {
     const int e = e0 + tid;
     const int c = e < E ? cnt[e] : 0;
-    int incl = c;
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int v = __shfl_up(incl, o, kWave);
-      if (tid >= o) incl += v;
-    }
+    const int incl = wave_incl_scan_i32(c);
     if (e < E) off[e] = base + incl - c;
     const uint64_t am = __ballot(c > 0);
     if (c > 0) {
@@ -90,7 +86,7 @@ __device__ __forceinline__ int scan_experts(const int* cnt, int* off, int* activ
       if (active_g != nullptr) active_g[pos] = e;
     }
     abase += popc64(am);
-    base += __shfl(incl, kWave - 1, kWave);
+    base += lane_value(incl, kWave - 1);
   }
   if (tid == 0) off[E] = base;
   return abase;
@@ -106,14 +102,10 @@ __device__ __forceinline__ void write_down_items(const ForwardParams& p, const i
     const int e = a < na ? active[a] : 0;
     const int c = a < na ? cnt[e] : 0;
     const int nb = (c + 15) / 16;
-    int incl = nb;
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int v = __shfl_up(incl, o, kWave);
-      if (tid >= o) incl += v;
-    }
+    const int incl = wave_incl_scan_i32(nb);
     for (int m = 0; m < nb; ++m)
       p.items[base + incl - nb + m] = make_int4(e, off[e] + 16 * m, min(16, c - 16 * m), 0);
-    base += __shfl(incl, kWave - 1, kWave);
+    base += lane_value(incl, kWave - 1);
   }
   if (tid == 0) *p.n_items = base;
 }
@@ -222,13 +214,14 @@ template <int KMAX>
 __device__ __forceinline__ void self_dispatch(const ForwardParams& p, SelfDispatch& sd, int tid) {
   const int E = p.E, k = p.k, T = p.T;
   const int words = (T + 31) / 32;
+  // the routing row first, so its latency overlaps the LDS clearing
+  int ev[KMAX];
+  uint32_t valid = 0u;
+  if (tid < T) valid = load_route_row<KMAX>(p.topk_idx + static_cast<size_t>(tid) * k, k, E, ev);
   for (int i = tid; i < E; i += 256) sd.cnt[i] = 0;
   for (int i = tid; i < E * words; i += 256) sd.mask[i] = 0u;
   __syncthreads();
-  int ev[KMAX];
-  uint32_t valid = 0u;
   if (tid < T) {
-    valid = load_route_row<KMAX>(p.topk_idx + static_cast<size_t>(tid) * k, k, E, ev);
 #pragma unroll
     for (int j = 0; j < KMAX; ++j) {
       if (valid & (1u << j)) {
@@ -763,6 +756,10 @@ __global__ __launch_bounds__(kColLanes / NB * kWave) void down_col_kernel(Forwar
   const int rowq = p.I * P::kElemBytes / 16;
   const int n_items = *p.n_items;
   const int n_rows = p.off[p.E];
+  // this wave's first item straight from the workspace, so the first stage's
+  // loads are in flight while the lists are staged in LDS
+  int4 first = make_int4(0, 0, 1, 0);
+  if (wave < n_items) first = p.items[wave];
   for (int i = tid; i < kWaves * T * kCols; i += kThreads) sh.acc[i] = 0.f;
   for (int i = tid; i < n_rows; i += kThreads) {
     const int slot = p.ent_slot[i];
@@ -770,7 +767,6 @@ __global__ __launch_bounds__(kColLanes / NB * kWave) void down_col_kernel(Forwar
     sh.gw[i] = p.topk_gate[slot];
   }
   for (int i = tid; i < n_items; i += kThreads) sh.items[i] = p.items[i];
-  __syncthreads();
 
   const uint4* wd = static_cast<const uint4*>(p.w_down);
   const uint4* act = static_cast<const uint4*>(p.act);
@@ -834,11 +830,10 @@ __global__ __launch_bounds__(kColLanes / NB * kWave) void down_col_kernel(Forwar
     }
     advance(c);
   };
+  Cursor lc{wave, 0, first.x, first.y, first.z}, cc{wave, 0, first.x, first.y, first.z};
+  if (nst > 0) load(w0, x0, lc);
+  __syncthreads();  // lists staged, accumulators cleared (advance reads the staged items)
   if (nst > 0) {
-    Cursor lc{wave, 0, 0, 0, 0}, cc{wave, 0, 0, 0, 0};
-    fetch(lc);
-    fetch(cc);
-    load(w0, x0, lc);
     advance(lc);
     int st = 0;
     for (; st + 2 < nst; st += 2) {
