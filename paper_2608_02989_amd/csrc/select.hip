@@ -39,7 +39,6 @@ struct SelShared {
   int code;
   int n_anchor, n_unat, n_R, n_pos, n_S, n_C, n_Sp, n_routed;
   int n_er, n_take, budget_a, m_star;
-  double Z;
   alignas(16) int Nd[kMaxTreeNodes];
   alignas(16) double alpha[kMaxTreeNodes];
   alignas(16) int votes[kMaxExperts];
@@ -57,6 +56,8 @@ struct SelShared {
   alignas(16) uint8_t routed[kMaxExperts];
   alignas(16) uint8_t resident[kMaxExperts];
   alignas(16) int rpart[kSelThreads];  // partial rank counts
+  alignas(16) int plist[kMaxExperts];     // compacted expert lists (index order) ...
+  alignas(16) double pval[kMaxExperts];   // ... and their utilities
 };
 
 // per-wave compaction scratch for top-k slot ordering
@@ -175,15 +176,6 @@ __device__ __forceinline__ void rank_all(const double* v, const uint8_t* flag, i
   }
 }
 
-// Deterministic workgroup sum of one double per expert (E <= 512): wave 0
-// adds lane-strided slices in index order, then a fixed butterfly.
-__device__ __forceinline__ double wg_sum_experts(const double* vals, int E, int wave, int lane) {
-  double s = 0.0;
-  if (wave == 0)
-    for (int e = lane; e < E; e += kWave) s += vals[e];
-  return wave == 0 ? wave_sum_f64(s) : 0.0;
-}
-
 // Workgroup counters without contention: each wave adds its ballot count (or
 // its lane sum) with a single LDS atomic.  Integer sums, so the order of the
 // atomics does not change the result.
@@ -300,8 +292,183 @@ __device__ __forceinline__ void restricted_node(const SelectParams& p, int t, in
 }
 
 // ---------------------------------------------------------------------------
+// Eq. 6, Sec. 3.3 and Eq. 7 for the self-sizing and fixed-budget modes, run
+// by one wave (lane l holds experts l, l + 64, ...) without workgroup
+// barriers.  Sums take the same per-lane order and wave reduction as the
+// workgroup path, integer counts are order-free, so the results are the same.
+// Writes inS, inSp, rankv (pruning order, -1 outside C), pv and the scalars.
+// ---------------------------------------------------------------------------
+template <int EPL>
+__device__ void eligible_set_wave(SelShared& sh, int mode, int E, int k, int bud, int removal_cap, bool prune,
+                                  int lane) {
+  const int kmin = min(k, E);
+  double u[EPL];
+  bool ok[EPL], inR[EPL], inS[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + kWave * i;
+    ok[i] = e < E;
+    u[i] = ok[i] ? sh.u[e] : 0.0;
+    inR[i] = ok[i] && sh.inR[e];
+    if (ok[i]) {
+      sh.inS[e] = sh.anchor[e];
+      sh.rankv[e] = -1;
+    }
+  }
+  const int n_anchor = sh.n_anchor, n_R = sh.n_R, n_pos = sh.n_pos;
+  int ner, take;
+  if (mode == MODE_SELF) {
+    // Z = sum over R of u^+ ; H = -sum q log q ; n_er = ceil(exp(H) - 1e-9)   (Eq. 6)
+    double zp = 0.0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i)
+      if (ok[i]) zp += (inR[i] && u[i] > 0.0) ? u[i] : 0.0;
+    const double Z = wave_sum_f64(zp);
+    double hp = 0.0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      if (!ok[i]) continue;
+      const double uu = (inR[i] && u[i] > 0.0) ? u[i] : 0.0;
+      double term = 0.0;
+      if (uu > 0.0 && Z > 0.0) {
+        const double q = uu / Z;
+        term = q * log(q);
+      }
+      hp += term;
+    }
+    const double hs = wave_sum_f64(hp);
+    ner = 0;
+    if (Z > 0.0) {
+      const double x = exp(-hs);
+      ner = static_cast<int>(ceil(x - 1e-9));
+      if (ner < 1) ner = 1;
+      if (ner > n_pos) ner = n_pos;
+    }
+    take = ner;
+    if (n_anchor + take < kmin) take = kmin - n_anchor;  // |S| >= k
+    if (take > n_R) take = n_R;
+  } else {
+    take = bud - n_anchor;
+    if (take < 0) take = 0;
+    if (take > n_R) take = n_R;
+    ner = take;
+  }
+  // S = A u first `take` of R in (u desc, index asc) order: members with u > 0
+  // (compacted in index order) ranked among themselves, then u = 0 members in
+  // index order if needed
+  int np = 0;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const bool f = inR[i] && u[i] > 0.0;
+    const uint64_t m = __ballot(f);
+    if (f) {
+      const int pos = np + popc64(m & lanes_below(lane));
+      sh.plist[pos] = lane + kWave * i;
+      sh.pval[pos] = u[i];
+    }
+    np += popc64(m);
+  }
+  wave_lds_sync();
+  for (int j0 = 0; j0 < np; j0 += kWave) {
+    const int j = j0 + lane;
+    const double vj = j < np ? sh.pval[j] : 0.0;
+    int r = 0;
+    for (int j2 = 0; j2 < np; ++j2) {
+      const double v2 = sh.pval[j2];
+      r += static_cast<int>((v2 > vj) | ((v2 == vj) & (j2 < j)));
+    }
+    if (j < np && r < take) sh.inS[sh.plist[j]] = 1;
+  }
+  if (take > np) {
+    int base = 0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const bool f = inR[i] && !(u[i] > 0.0);
+      const uint64_t m = __ballot(f);
+      if (f && np + base + popc64(m & lanes_below(lane)) < take) sh.inS[lane + kWave * i] = 1;
+      base += popc64(m);
+    }
+  }
+  wave_lds_sync();
+  // |S|, a(S) = votes of the experts outside S
+  int ns = 0, as = 0;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + kWave * i;
+    inS[i] = ok[i] && sh.inS[e] != 0;
+    ns += inS[i] ? 1 : 0;
+    as += (ok[i] && !inS[i]) ? sh.votes[e] : 0;
+  }
+  const int nS = wave_sum_i32(ns), aS = wave_sum_i32(as);
+  int m_star = 0, nC = 0;
+  if (prune) {
+    // C = nonresident members of S ordered by (u asc, index asc)   (Sec. 3.4)
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const bool f = inS[i] && !sh.resident[lane + kWave * i];
+      const uint64_t m = __ballot(f);
+      if (f) {
+        const int pos = nC + popc64(m & lanes_below(lane));
+        sh.plist[pos] = lane + kWave * i;
+        sh.pval[pos] = u[i];
+      }
+      nC += popc64(m);
+    }
+    wave_lds_sync();
+    for (int j0 = 0; j0 < nC; j0 += kWave) {
+      const int j = j0 + lane;
+      const double vj = j < nC ? sh.pval[j] : 0.0;
+      int r = 0;
+      for (int j2 = 0; j2 < nC; ++j2) {
+        const double v2 = sh.pval[j2];
+        r += static_cast<int>((v2 < vj) | ((v2 == vj) & (j2 < j)));
+      }
+      if (j < nC) {
+        const int e = sh.plist[j];
+        sh.rankv[e] = r;
+        sh.pv[r] = sh.votes[e];
+      }
+    }
+    wave_lds_sync();
+    // m* = longest prefix with sum v <= a(S), |S| - m >= k, m <= removal cap   (Eq. 7);
+    // votes are >= 0, so the prefix sums only grow and the admissible m form a prefix
+    int limit = nC;
+    if (nS - k < limit) limit = nS - k;
+    if (removal_cap < limit) limit = removal_cap;
+    if (limit < 0) limit = 0;
+    int base = 0;
+    for (int r0 = 0; r0 < limit; r0 += kWave) {
+      const int r = r0 + lane;
+      const int v = r < limit ? sh.pv[r] : 0;
+      const int cum = base + wave_incl_scan_i32(v);
+      const int cnt = popc64(__ballot(r < limit && cum <= aS));
+      m_star += cnt;
+      if (cnt < min(kWave, limit - r0)) break;
+      base = lane_value(cum, kWave - 1);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + kWave * i;
+    if (ok[i]) {
+      const int rk = sh.rankv[e];
+      sh.inSp[e] = inS[i] && !(rk >= 0 && rk < m_star);
+    }
+  }
+  if (lane == 0) {
+    sh.n_er = ner;
+    sh.n_take = take;
+    sh.n_S = nS;
+    sh.budget_a = aS;
+    sh.n_C = nC;
+    sh.m_star = m_star;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // eligible set of one tree
 // ---------------------------------------------------------------------------
+template <int EPL>
 __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeOffsets offs) {
   __shared__ SelShared sh;
   const int tid = threadIdx.x;
@@ -422,126 +589,46 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
   const int kmin = min(k, E);
   const int bud = p.budget < kmin ? kmin : (p.budget > E ? E : p.budget);
 
-  if (mode == MODE_SELF) {
-    // Z = sum over R of u^+ ; H = -sum q log q ; n_er = ceil(exp(H) - 1e-9)   (Eq. 6)
-    if (tid < E) sh.dense[tid] = (sh.inR[tid] && sh.u[tid] > 0.0) ? sh.u[tid] : 0.0;
-    __syncthreads();
-    const double Z = wg_sum_experts(sh.dense, E, wave, lane);
-    if (tid == 0) sh.Z = Z;
-    __syncthreads();
-    const double Zs = sh.Z;
-    if (tid < E) {
-      const double uu = sh.dense[tid];
-      double term = 0.0;
-      if (uu > 0.0 && Zs > 0.0) {
-        const double q = uu / Zs;
-        term = q * log(q);
-      }
-      sh.dense[kMaxExperts + tid] = term;
-    }
-    __syncthreads();
-    const double hs = wg_sum_experts(sh.dense + kMaxExperts, E, wave, lane);
-    if (tid == 0) {
-      int ner = 0;
-      if (Zs > 0.0) {
-        const double x = exp(-hs);
-        ner = static_cast<int>(ceil(x - 1e-9));
-        if (ner < 1) ner = 1;
-        if (ner > sh.n_pos) ner = sh.n_pos;
-      }
-      sh.n_er = ner;
-      int take = ner;
-      if (sh.n_anchor + take < kmin) take = kmin - sh.n_anchor;  // |S| >= k
-      if (take > sh.n_R) take = sh.n_R;
-      sh.n_take = take;
-    }
-  } else if (mode == MODE_FIXED) {
-    if (tid == 0) {
-      int take = bud - sh.n_anchor;
-      if (take < 0) take = 0;
-      if (take > sh.n_R) take = sh.n_R;
-      sh.n_er = take;
-      sh.n_take = take;
-    }
-  } else if (mode == MODE_MOESPEC || mode == MODE_COUNT) {
-    // MoE-Spec: router mass summed over the block; Count-B: natural votes
-    if (tid < E) {
-      double score = 0.0;
-      if (mode == MODE_MOESPEC) {
-#pragma unroll 8
-        for (int tl = 0; tl < Tb; ++tl) score += p.ws_rfull[static_cast<size_t>(t_begin + tl) * E + tid];
-      } else {
-        score = static_cast<double>(sh.votes[tid]);
-      }
-      sh.score[tid] = score;
-      sh.inC[tid] = 1;  // every expert competes
-    }
-  }
-  __syncthreads();
-
   if (mode == MODE_SELF || mode == MODE_FIXED) {
-    // S = A u first n_take of R in (u desc, index asc) order
-    rank_all<true>(sh.u, sh.inR, E, sh.rankv, sh.rpart, tid);
+    // Eq. 6, S, |S|, a(S) and the Eq. 7 pruning in one wave
+    if (wave == 0) eligible_set_wave<EPL>(sh, mode, E, k, bud, p.removal_cap, has_mask, lane);
     __syncthreads();
-    if (tid < E) sh.inS[tid] = sh.anchor[tid] || sh.rankv[tid] < sh.n_take;
-  } else if (mode == MODE_ALL) {
-    if (tid < E) sh.inS[tid] = 1;
   } else {
-    rank_all<true>(sh.score, sh.inC, E, sh.rankv, sh.rpart, tid);
-    __syncthreads();
-    if (tid < E) sh.inS[tid] = sh.rankv[tid] < bud;
-  }
-  __syncthreads();
-  if (tid < E) sh.rankv[tid] = 0;
-
-  // |S|, a(S)
-  {
-    const bool in_e = tid < E;
-    const bool inS = in_e && sh.inS[tid];
-    if (in_e) sh.inC[tid] = 0;
-    wg_count(inS, &sh.n_S, lane);
-    wg_add((in_e && !inS) ? sh.votes[tid] : 0, &sh.budget_a, lane);
-    wg_count((mode == MODE_MOESPEC || mode == MODE_COUNT) && inS && !sh.anchor[tid], &sh.n_er, lane);
-  }
-  __syncthreads();
-  if (mode == MODE_ALL && tid == 0) {
-    sh.n_er = E - sh.n_anchor;
-    sh.budget_a = 0;
-  }
-
-  const bool prune = has_mask && (mode == MODE_SELF || mode == MODE_FIXED);
-  if (prune) {
-    // C = nonresident members of S ordered by (u asc, index asc)   (Sec. 3.4)
-    {
-      const bool c = tid < E && sh.inS[tid] && !sh.resident[tid];
-      if (tid < E) sh.inC[tid] = c;
-      wg_count(c, &sh.n_C, lane);
-    }
-    __syncthreads();
-    rank_all<false>(sh.u, sh.inC, E, sh.rankv, sh.rpart, tid);
-    __syncthreads();
-    if (tid < E) {
-      if (sh.inC[tid]) sh.pv[sh.rankv[tid]] = sh.votes[tid];
-      else sh.rankv[tid] = -1;
-    }
-    __syncthreads();
-    // m* = longest prefix with sum v <= a(S), |S| - m >= k, m <= removal cap   (Eq. 7)
-    if (tid == 0) {
-      int limit = sh.n_C;
-      if (sh.n_S - k < limit) limit = sh.n_S - k;
-      if (p.removal_cap < limit) limit = p.removal_cap;
-      if (limit < 0) limit = 0;
-      int m = 0, acc = 0;
-      while (m < limit && acc + sh.pv[m] <= sh.budget_a) {
-        acc += sh.pv[m];
-        ++m;
+    if (mode == MODE_MOESPEC || mode == MODE_COUNT) {
+      // MoE-Spec: router mass summed over the block; Count-B: natural votes
+      if (tid < E) {
+        double score = 0.0;
+        if (mode == MODE_MOESPEC) {
+#pragma unroll 8
+          for (int tl = 0; tl < Tb; ++tl) score += p.ws_rfull[static_cast<size_t>(t_begin + tl) * E + tid];
+        } else {
+          score = static_cast<double>(sh.votes[tid]);
+        }
+        sh.score[tid] = score;
+        sh.inC[tid] = 1;  // every expert competes
       }
-      sh.m_star = m;
+      __syncthreads();
+      rank_all<true>(sh.score, sh.inC, E, sh.rankv, sh.rpart, tid);
+      __syncthreads();
+      if (tid < E) sh.inS[tid] = sh.rankv[tid] < bud;
+    } else {  // natural routing: S = [E]
+      if (tid < E) sh.inS[tid] = 1;
     }
     __syncthreads();
-    if (tid < E) sh.inSp[tid] = sh.inS[tid] && !(sh.rankv[tid] >= 0 && sh.rankv[tid] < sh.m_star);
-  } else {
-    if (tid < E) sh.inSp[tid] = sh.inS[tid];
+    // |S|, a(S)
+    {
+      const bool in_e = tid < E;
+      const bool inS = in_e && sh.inS[tid];
+      wg_count(inS, &sh.n_S, lane);
+      wg_add((in_e && !inS) ? sh.votes[tid] : 0, &sh.budget_a, lane);
+      wg_count(mode != MODE_ALL && inS && !sh.anchor[tid], &sh.n_er, lane);
+      if (in_e) sh.inSp[tid] = inS;  // no pruning outside the self-sizing / fixed-budget modes
+    }
+    __syncthreads();
+    if (mode == MODE_ALL && tid == 0) {
+      sh.n_er = E - sh.n_anchor;
+      sh.budget_a = 0;
+    }
   }
   __syncthreads();
 
@@ -610,7 +697,7 @@ template <int EPL>
 hipError_t launch_select_epl(const SelectParams& p, const TreeOffsets& offs, hipStream_t stream) {
   const int node_blocks = (p.T + kNodeWaves - 1) / kNodeWaves;
   if (node_blocks > 0) natural_kernel<EPL><<<node_blocks, kNodeWaves * kWave, 0, stream>>>(p);
-  tree_kernel<<<p.B, kSelThreads, 0, stream>>>(p, offs);
+  tree_kernel<EPL><<<p.B, kSelThreads, 0, stream>>>(p, offs);
   if (node_blocks > 0) restricted_kernel<EPL><<<node_blocks, kNodeWaves * kWave, 0, stream>>>(p, offs);
   return hipGetLastError();
 }
