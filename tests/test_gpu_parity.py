@@ -292,6 +292,24 @@ def test_forward_parity_ragged_and_hot_expert(gpu, dtype, T):
     assert np.all(got[6] == 0.0)
 
 
+# forward path limits: k > 8 in the in-LDS dispatch, exactly 256 tokens / 2048
+# slots (largest column-tile block), 257 tokens (per-slot pass), E = 48
+@pytest.mark.parametrize("T,k,E,dtype", [(40, 32, 64, "bf16"), (37, 12, 48, "f32"), (256, 8, 64, "bf16"),
+                                         (257, 8, 64, "bf16")])
+def test_forward_parity_path_limits(gpu, T, k, E, dtype):
+    cfg = W.LayerConfig("limits", 95 + T + k, dtype, T=T, B=1, H=256, E=E, k=k, I=128, depth_max=6,
+                        commit_rule="depth_sibling", hidden_std=1.0)
+    rng = np.random.default_rng(T * 100 + k)
+    h32 = rng.standard_normal((T, cfg.H)).astype(np.float32)
+    idx = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    gate = rng.random((T, k)).astype(np.float32)
+    say(f"forward limits T={T} k={k} E={E} dtype={dtype}")
+    got, h64, (wg, wu, wd) = forward_case(cfg, idx, gate, h32)
+    ref = O.moe_forward_grouped(h64, wg, wu, wd, idx, gate, cfg.dtype)
+    err = normwise_rel(got, ref)
+    assert err <= FWD_TOL[cfg.dtype], err
+
+
 def test_pack_router_layout_documented(gpu):
     # values encode (e, h); rows past E are zero
     E, H = 20, 48
