@@ -251,12 +251,11 @@ __global__ __launch_bounds__(kNodeWaves * kWave) void natural_kernel(SelectParam
 // ---------------------------------------------------------------------------
 // restricted top-k over the eligible set and renormalised gates of node t
 // (one wave).  elig[e] != 0 marks e in S'.  Experts that receive the node are
-// counted into stats[b][9] once each, through the tree's bitmask in the
-// workspace.
+// marked in `routed` (an LDS bitmask of the workgroup).
 // ---------------------------------------------------------------------------
 template <int EPL>
-__device__ __forceinline__ void restricted_node(const SelectParams& p, int t, int b, const uint8_t* elig, int lane,
-                                                uint32_t* sk, int* se, float* sz) {
+__device__ __forceinline__ void restricted_node(const SelectParams& p, int t, const uint8_t* elig, int lane,
+                                                uint32_t* sk, int* se, float* sz, uint32_t* routed) {
   const int E = p.E, k = p.k;
   float zv[EPL];
   uint32_t key[EPL];
@@ -279,11 +278,7 @@ __device__ __forceinline__ void restricted_node(const SelectParams& p, int t, in
     const int e = se[lane];
     orow[slot] = e;
     grow[slot] = static_cast<float>(w / ws);
-    if (p.stats != nullptr) {
-      const uint32_t bit = 1u << (e & 31);
-      const uint32_t old = atomicOr(&p.ws_routed[b * kRoutedWords + (e >> 5)], bit);
-      if (!(old & bit)) atomicAdd(&p.stats[b * kNumStats + 9], 1);
-    }
+    atomicOr(&routed[e >> 5], 1u << (e & 31));
   } else if (lane < k) {
     orow[lane] = -1;  // fewer eligible experts than k (an invalid tree has none)
     grow[lane] = 0.0f;
@@ -654,21 +649,53 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
 // ---------------------------------------------------------------------------
 // restricted top-k, one wave per node
 // ---------------------------------------------------------------------------
+// Routed experts are counted per tree into stats[b][9]: each wave marks its
+// node's experts in an LDS bitmask; the masks of the workgroup's nodes are
+// merged per tree and added to the tree's workspace bitmask with one atomic
+// per nonzero word, and the newly set bits with one atomic per tree (per-slot
+// global atomics on a handful of words serialize).
 template <int EPL>
 __global__ __launch_bounds__(kNodeWaves * kWave) void restricted_kernel(SelectParams p, TreeOffsets offs) {
   __shared__ NodeScratch ns;
+  __shared__ uint32_t routed[kNodeWaves][kRoutedWords];
+  __shared__ int tree_of[kNodeWaves];
   const int wave = wave_id(), lane = lane_id();
   const int t = blockIdx.x * kNodeWaves + wave;
-  if (t >= p.T) return;
-  // tree of node t: the b with o[b] <= t < o[b+1] (empty trees are skipped)
-  int lo = 0, hi = p.B - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (offs.o[mid] <= t) lo = mid;
-    else hi = mid - 1;
+  if (lane < kRoutedWords) routed[wave][lane] = 0u;
+  int b = -1;
+  if (t < p.T) {
+    // tree of node t: the b with o[b] <= t < o[b+1] (empty trees are skipped)
+    int lo = 0, hi = p.B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (offs.o[mid] <= t) lo = mid;
+      else hi = mid - 1;
+    }
+    b = lo;
+    wave_lds_sync();
+    restricted_node<EPL>(p, t, p.eligible + static_cast<size_t>(b) * p.E, lane, ns.sk[wave], ns.se[wave],
+                         ns.sz[wave], routed[wave]);
   }
-  restricted_node<EPL>(p, t, lo, p.eligible + static_cast<size_t>(lo) * p.E, lane, ns.sk[wave], ns.se[wave],
-                       ns.sz[wave]);
+  if (lane == 0) tree_of[wave] = b;
+  if (p.stats == nullptr) return;
+  __syncthreads();
+  if (wave == 0) {
+    const int words = (p.E + 31) / 32;
+    for (int w0 = 0; w0 < kNodeWaves; ++w0) {
+      const int tb = tree_of[w0];
+      bool first = tb >= 0;
+      for (int w1 = 0; w1 < w0; ++w1) first = first && tree_of[w1] != tb;
+      if (!first) continue;  // this tree was merged at its first wave
+      uint32_t m = 0u;
+      if (lane < words)
+        for (int w1 = w0; w1 < kNodeWaves; ++w1)
+          if (tree_of[w1] == tb) m |= routed[w1][lane];
+      int fresh = 0;
+      if (m != 0u) fresh = __popc(m & ~atomicOr(&p.ws_routed[tb * kRoutedWords + lane], m));
+      fresh = wave_sum_i32(fresh);
+      if (lane == 0 && fresh) atomicAdd(&p.stats[tb * kNumStats + 9], fresh);
+    }
+  }
 }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
