@@ -16,6 +16,7 @@ Prints one JSON line:
 from __future__ import annotations
 
 import argparse
+import itertools
 import json
 import os
 import sys
@@ -440,15 +441,19 @@ def cpu_baseline(cfg, layers, blocks, budget_s, ebytes, log):
     except Exception:
         threads = os.cpu_count() or 1
     elapsed, nbytes, n = 0.0, 0.0, 0
-    for b, B_ in enumerate(blocks):
-        blk = B_["host"]
+    prepared = set()
+    # cycle over the blocks until the time budget is used (a bounded sample)
+    for b in itertools.cycle(range(len(blocks))):
+        blk = blocks[b]["host"]
         h64 = (O.widen_bf16(W.bf16_round(blk.hidden)) if cfg.dtype == "bf16"
                else blk.hidden.astype(np.float64))
-        # weights needed by this block go to host memory before the clock starts
-        z_pre = O.route(h64, rw).astype(np.float32)
-        pre = O.select(z_pre, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, resident=blk.resident)
-        for e in np.unique(pre["idx"][pre["idx"] >= 0]):
-            fetch(int(e))
+        if b not in prepared:
+            # weights needed by this block go to host memory before the clock starts
+            z_pre = O.route(h64, rw).astype(np.float32)
+            pre = O.select(z_pre, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, resident=blk.resident)
+            for e in np.unique(pre["idx"][pre["idx"] >= 0]):
+                fetch(int(e))
+            prepared.add(b)
         t1 = time.perf_counter()
         z = O.route(h64, rw).astype(np.float32)
         sel = O.select(z, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, resident=blk.resident)
@@ -461,8 +466,9 @@ def cpu_baseline(cfg, layers, blocks, budget_s, ebytes, log):
     del wg, wu, wd
     log(f"cpu oracle: {n} blocks in {elapsed:.1f}s")
     return {"value": round(nbytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} blocks of {cfg.name} (layer 0), route+select+grouped forward in fp64 numpy, "
-                      f"{elapsed:.1f} s", "latency_us": round(elapsed / n * 1e6, 1)}
+            "sample": f"{n} block passes over {len(prepared)} seeded blocks of {cfg.name} (layer 0), "
+                      f"route+select+grouped forward in fp64 numpy, {elapsed:.1f} s",
+            "latency_us": round(elapsed / n * 1e6, 1)}
 
 
 if __name__ == "__main__":
