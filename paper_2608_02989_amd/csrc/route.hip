@@ -1,6 +1,7 @@
 // Router logits z_t = W_r h_t (Sec. 3.1): an fp32 [T,H] x [E,H]^T product on
-// the fp32 MFMA (v_mfma_f32_16x16x4f32), one 16-token x 16-expert tile per
-// workgroup of 16 waves, each wave reducing a slice of H.
+// the fp32 MFMA (v_mfma_f32_16x16x4f32), one 16-token x 16-expert tile (or
+// 16 x 8 for small grids) per workgroup of 16 waves, each wave reducing a
+// slice of H.
 //
 // Both operands are read with whole-cache-line accesses: the router weights
 // come pre-packed in MFMA fragment order (one contiguous 1 KiB read per
@@ -49,10 +50,16 @@ __device__ __forceinline__ float4 widen4(const uint16_t* p) {
                      __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
 }
 
-// grid (ceil(E/16), ceil(T/16)), block 1024.  Lane (r, g) of a wave: token row
-// t0 + r of the A tile and expert 16 et + r of the B tile; component j of K
-// slice g of chunk c is column 16c + 4g + j (same for both operands).
-template <typename TIn>
+// grid (ceil(E/EW), ceil(T/16)), block 1024, EW = 16 or 8 experts per
+// workgroup.  Lane (r, g) of a wave: token row t0 + r of the A tile and expert
+// row r of the B tile; component j of K slice g of chunk c is column
+// 16c + 4g + j (same for both operands).  With EW = 8 a workgroup reads one
+// half of each 16-row weight fragment (rows 0-7 or 8-15: four whole 128-byte
+// lines of the 1 KiB fragment), lanes r >= 8 repeat lanes r - 8 and their
+// output columns are dropped; twice the workgroups then share the weights,
+// which matters when only a few tiles exist (the per-CU read rate bounds a
+// small grid).
+template <typename TIn, int EW>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(const TIn* __restrict__ hidden,
                                                              const float4* __restrict__ wp, int T, int H, int E,
                                                              float* __restrict__ logits) {
@@ -66,9 +73,11 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(const TIn* __restr
   const int wave = wave_id();
   const int lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
-  const int et = blockIdx.x, t0 = blockIdx.y * 16;
+  const int e0 = blockIdx.x * EW, t0 = blockIdx.y * 16;
   const int nchunk = H / 16;
-  const float4* wrow = wp + static_cast<size_t>(et) * nchunk * kWave + lane;
+  // fragment lane holding expert row (e0 % 16) + (r % EW) for K slice g
+  const int wl = (e0 % 16) + (r % EW) + 16 * g;
+  const float4* wrow = wp + static_cast<size_t>(e0 / 16) * nchunk * kWave + wl;
 
   floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
   for (int kb0 = 0; kb0 < H; kb0 += kBlockCols) {
@@ -127,8 +136,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(const TIn* __restr
       s[2] += q[2];
       s[3] += q[3];
     }
-    const int e = et * 16 + r;
-    if (e < E) {
+    const int e = e0 + r;
+    if (r < EW && e < E) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int tt = t0 + 4 * g + i;
@@ -154,13 +163,27 @@ hipError_t launch_pack_router(const float* src, int E, int H, float* dst, hipStr
 
 hipError_t launch_route(const void* hidden, int hidden_is_bf16, const float* router_packed, int T, int H, int E,
                         float* logits, hipStream_t stream) {
-  dim3 grid((E + 15) / 16, (T + 15) / 16);
   const float4* wp = reinterpret_cast<const float4*>(router_packed);
-  if (hidden_is_bf16)
-    route_kernel<uint16_t><<<grid, kRouteThreads, 0, stream>>>(static_cast<const uint16_t*>(hidden), wp, T, H, E,
-                                                                logits);
-  else
-    route_kernel<float><<<grid, kRouteThreads, 0, stream>>>(static_cast<const float*>(hidden), wp, T, H, E, logits);
+  const int ttiles = (T + 15) / 16;
+  // small grids: 8 experts per workgroup, so twice as many CUs read the weights
+  const bool half = ((E + 15) / 16) * ttiles < 128;
+  if (half) {
+    dim3 grid((E + 7) / 8, ttiles);
+    if (hidden_is_bf16)
+      route_kernel<uint16_t, 8><<<grid, kRouteThreads, 0, stream>>>(static_cast<const uint16_t*>(hidden), wp, T, H,
+                                                                     E, logits);
+    else
+      route_kernel<float, 8><<<grid, kRouteThreads, 0, stream>>>(static_cast<const float*>(hidden), wp, T, H, E,
+                                                                  logits);
+  } else {
+    dim3 grid((E + 15) / 16, ttiles);
+    if (hidden_is_bf16)
+      route_kernel<uint16_t, 16><<<grid, kRouteThreads, 0, stream>>>(static_cast<const uint16_t*>(hidden), wp, T, H,
+                                                                      E, logits);
+    else
+      route_kernel<float, 16><<<grid, kRouteThreads, 0, stream>>>(static_cast<const float*>(hidden), wp, T, H, E,
+                                                                   logits);
+  }
   return hipGetLastError();
 }
 

@@ -52,7 +52,7 @@ def u8(a):
 # route
 # ---------------------------------------------------------------------------
 ROUTE_CASES = [("fp32_small", None, None), ("qwen3_30b_a3b", None, None), ("wide_offload", None, None),
-               ("batched_8x64", None, None), ("qwen3_30b_a3b", 37, 100)]
+               ("batched_8x64", None, None), ("qwen3_30b_a3b", 37, 100), ("batched_8x64", None, 100)]
 
 
 @pytest.mark.parametrize("name,T,E", ROUTE_CASES)
