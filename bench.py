@@ -166,7 +166,7 @@ def main():
         ops.select(logits, B_["parent"], B_["depth"], B_["prob"], B_["offs"], L_.k, L_.beta, L_.mode,
                    L_.budget, L_.removal_cap, B_["resident"], workspace=L_.sel_ws, outputs=outs, stream=stream)
         ev[0].record(stream)
-        ops.moe_forward(B_["h"], L_.wg, L_.wu, L_.wd, outs["idx"], outs["gate"], out=L_.out[:T],
+        ops.moe_forward(B_["h"], L_.wgu, L_.wd, outs["idx"], outs["gate"], out=L_.out[:T],
                         workspace=L_.fwd_ws, stream=stream)
         ev[1].record(stream)
 

@@ -178,11 +178,35 @@ int32_t acceptmoe_select(const float* logits, const int32_t* parent, const int32
  *
  *   src  [E, N, K] device, dtype F32 or BF16;  dst packed, device, same size,
  *   must not overlap src.  Requires N % 16 == 0 and K % (64 / sizeof(elem)) == 0.
- * Gate and up stacks are [E, I, H] (N = I, K = H); the down stack is [E, H, I].
+ * The down stack [E, H, I] is packed this way (N = H, K = I); the gate and
+ * up stacks go through acceptmoe_pack_gate_up_weights.
  */
 size_t acceptmoe_packed_weights_bytes(int32_t dtype, int32_t E, int32_t N, int32_t K);
 int32_t acceptmoe_pack_expert_weights(const void* src, int32_t dtype, int32_t E, int32_t N,
                                       int32_t K, void* dst, void* stream);
+
+/*
+ * acceptmoe_packed_gate_up_bytes -- bytes of a packed gate/up pair of stacks.
+ * acceptmoe_pack_gate_up_weights -- packs the gate and up stacks [E, I, H]
+ * (the W_g and W_u of Eq. 2) into one buffer laid out for the gate/up pass:
+ * for every expert e, every pair p of 16-row tiles (rows 32p .. 32p+31 of I)
+ * and every K chunk c (64 bytes of each row), four 1 KiB fragments follow
+ * each other -- gate tile 2p, gate tile 2p+1, up tile 2p, up tile 2p+1 --
+ * each in the fragment order of acceptmoe_pack_expert_weights (lane L holds
+ * row L % 16, bytes 16*(L / 16) .. +15 of the chunk).  Fragment
+ * ((e * ceil(I/32) + p) * (H*eb/64) + c) * 4 + f starts at byte 1024 times
+ * that index.  When I/16 is odd the last pair's second tiles are zeros, so the
+ * size is E * ceil(I/32) * 32 * H * eb * 2 bytes (exactly the two stacks when
+ * I % 32 == 0).  A one-time, load-time step.
+ *
+ *   w_gate, w_up  [E, I, H] device, dtype F32 or BF16 (eb = 4 or 2 bytes)
+ *   dst           device, acceptmoe_packed_gate_up_bytes(dtype, E, I, H)
+ *                 bytes, must not overlap either source
+ *   Requires I % 16 == 0 and H % (64 / eb) == 0; pointers 16-byte aligned.
+ */
+size_t acceptmoe_packed_gate_up_bytes(int32_t dtype, int32_t E, int32_t I, int32_t H);
+int32_t acceptmoe_pack_gate_up_weights(const void* w_gate, const void* w_up, int32_t dtype,
+                                       int32_t E, int32_t I, int32_t H, void* dst, void* stream);
 
 /*
  * acceptmoe_moe_forward_workspace_size -- device workspace bytes for
@@ -198,8 +222,8 @@ size_t acceptmoe_moe_forward_workspace_size(int32_t T, int32_t H, int32_t I, int
  * Only experts that receive at least one token are read, each exactly once.
  *
  *   hidden        [T, H] device, element type `dtype`
- *   w_gate, w_up  packed [E, I, H] stacks (acceptmoe_pack_expert_weights), `dtype`
- *   w_down        packed [E, H, I] stack, `dtype`
+ *   w_gate_up     gate and up stacks packed by acceptmoe_pack_gate_up_weights, `dtype`
+ *   w_down        packed [E, H, I] stack (acceptmoe_pack_expert_weights), `dtype`
  *   topk_idx      [T, k] int32 device; entries outside [0, E) are skipped, and an
  *                 expert repeated within a row is used once (at its first slot)
  *   topk_gate     [T, k] fp32 device
@@ -217,9 +241,9 @@ size_t acceptmoe_moe_forward_workspace_size(int32_t T, int32_t H, int32_t I, int
  * two) the two fp32 halves added onto zero, which commutes; larger blocks sum
  * the k contributions of a token in slot order.
  */
-int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_gate,
-                              const void* w_up, const void* w_down, int32_t T, int32_t H,
-                              int32_t I, int32_t E, int32_t k, const int32_t* topk_idx,
+int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_gate_up,
+                              const void* w_down, int32_t T, int32_t H, int32_t I, int32_t E,
+                              int32_t k, const int32_t* topk_idx,
                               const float* topk_gate, float* out, void* workspace,
                               size_t workspace_bytes, void* stream);
 

@@ -46,7 +46,9 @@ SIGNATURES = {
     "acceptmoe_packed_weights_bytes": (_sz, [_i32, _i32, _i32, _i32]),
     "acceptmoe_pack_expert_weights": (_i32, [_vp, _i32, _i32, _i32, _i32, _vp, _vp]),
     "acceptmoe_moe_forward_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
-    "acceptmoe_moe_forward": (_i32, [_vp, _i32, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp,
+    "acceptmoe_packed_gate_up_bytes": (_sz, [_i32, _i32, _i32, _i32]),
+    "acceptmoe_pack_gate_up_weights": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp]),
+    "acceptmoe_moe_forward": (_i32, [_vp, _i32, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp,
                                      _vp, _vp, _sz, _vp]),
     "acceptmoe_last_error": (ctypes.c_char_p, []),
     "acceptmoe_version": (_i32, []),

@@ -37,7 +37,7 @@ extern "C" {
 
 const char* acceptmoe_last_error(void) { return g_err; }
 
-int32_t acceptmoe_version(void) { return 100; }
+int32_t acceptmoe_version(void) { return 200; }
 
 // ---------------------------------------------------------------------------
 size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H) {
@@ -186,6 +186,36 @@ int32_t acceptmoe_pack_expert_weights(const void* src, int32_t dtype, int32_t E,
   return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "pack launch");
 }
 
+size_t acceptmoe_packed_gate_up_bytes(int32_t dtype, int32_t E, int32_t I, int32_t H) {
+  if ((dtype != ACCEPTMOE_F32 && dtype != ACCEPTMOE_BF16) || E < 1 || I < 1 || H < 1) return 0;
+  return amoe::packed_gate_up_bytes(dtype == ACCEPTMOE_BF16, E, I, H);
+}
+
+int32_t acceptmoe_pack_gate_up_weights(const void* w_gate, const void* w_up, int32_t dtype, int32_t E, int32_t I,
+                                       int32_t H, void* dst, void* stream) {
+  clear_err();
+  if (dtype != ACCEPTMOE_F32 && dtype != ACCEPTMOE_BF16)
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "pack_gate_up: unknown dtype %d", dtype);
+  if (E < 1 || I < 1 || H < 1) return fail(ACCEPTMOE_ERR_INVALID_ARG, "pack_gate_up: E, I, H must be >= 1");
+  const int kf = 64 / elem_bytes(dtype);
+  if (I % 16 != 0 || H % kf != 0)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "pack_gate_up: need I %% 16 == 0 and H %% %d == 0 (I=%d H=%d)", kf, I, H);
+  if (!w_gate || !w_up || !dst) return fail(ACCEPTMOE_ERR_INVALID_ARG, "pack_gate_up: null pointer");
+  if (!aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(dst, 16))
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "pack_gate_up: w_gate, w_up and dst must be 16-byte aligned");
+  const size_t src_bytes = static_cast<size_t>(E) * I * H * elem_bytes(dtype);
+  const size_t dst_bytes = amoe::packed_gate_up_bytes(dtype == ACCEPTMOE_BF16, E, I, H);
+  const char* d = static_cast<const char*>(dst);
+  for (const void* src : {w_gate, w_up}) {
+    const char* s = static_cast<const char*>(src);
+    if (s < d + dst_bytes && d < s + src_bytes)
+      return fail(ACCEPTMOE_ERR_INVALID_ARG, "pack_gate_up: a source overlaps dst");
+  }
+  hipError_t e = amoe::launch_pack_gate_up(w_gate, w_up, dtype == ACCEPTMOE_BF16, E, I, H, dst,
+                                           static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "pack_gate_up launch");
+}
+
 // ---------------------------------------------------------------------------
 size_t acceptmoe_moe_forward_workspace_size(int32_t T, int32_t H, int32_t I, int32_t E, int32_t k,
                                             int32_t dtype) {
@@ -194,9 +224,8 @@ size_t acceptmoe_moe_forward_workspace_size(int32_t T, int32_t H, int32_t I, int
   return amoe::forward_workspace_bytes(T, H, I, E, k, dtype == ACCEPTMOE_BF16);
 }
 
-int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_gate, const void* w_up,
-                              const void* w_down, int32_t T, int32_t H, int32_t I, int32_t E, int32_t k,
-                              const int32_t* topk_idx, const float* topk_gate, float* out, void* workspace,
+int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_gate_up, const void* w_down,
+                              int32_t T, int32_t H, int32_t I, int32_t E, int32_t k, const int32_t* topk_idx, const float* topk_gate, float* out, void* workspace,
                               size_t workspace_bytes, void* stream) {
   clear_err();
   if (dtype != ACCEPTMOE_F32 && dtype != ACCEPTMOE_BF16)
@@ -213,10 +242,9 @@ int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_g
   if (T == 0) return ACCEPTMOE_OK;
   if (static_cast<long long>(T) * k > (1ll << 30))
     return fail(ACCEPTMOE_ERR_UNSUPPORTED, "forward: T*k too large");
-  if (!hidden || !w_gate || !w_up || !w_down || !topk_idx || !topk_gate || !out)
+  if (!hidden || !w_gate_up || !w_down || !topk_idx || !topk_gate || !out)
     return fail(ACCEPTMOE_ERR_INVALID_ARG, "forward: null pointer");
-  if (!aligned(hidden, 16) || !aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(w_down, 16) ||
-      !aligned(out, 16))
+  if (!aligned(hidden, 16) || !aligned(w_gate_up, 16) || !aligned(w_down, 16) || !aligned(out, 16))
     return fail(ACCEPTMOE_ERR_INVALID_ARG, "forward: hidden, weights and out must be 16-byte aligned");
   const size_t need = amoe::forward_workspace_bytes(T, H, I, E, k, dtype == ACCEPTMOE_BF16);
   if (workspace == nullptr || workspace_bytes < need)
@@ -226,8 +254,7 @@ int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_g
   amoe::ForwardParams p;
   std::memset(&p, 0, sizeof p);
   p.hidden = hidden;
-  p.w_gate = w_gate;
-  p.w_up = w_up;
+  p.w_gate_up = w_gate_up;
   p.w_down = w_down;
   p.topk_idx = topk_idx;
   p.topk_gate = topk_gate;

@@ -49,6 +49,30 @@ __global__ void pack_kernel(const uint4* __restrict__ src, uint4* __restrict__ d
   }
 }
 
+// gate and up stacks [E, I, H] -> [E][I/32 tile pairs][K/KF][4][64 lanes][16 B]:
+// fragments gate 2p, gate 2p+1, up 2p, up 2p+1 of each K chunk side by side;
+// the second tile of the last pair is zero when I/16 is odd.
+__global__ void pack_gate_up_kernel(const uint4* __restrict__ gate, const uint4* __restrict__ up,
+                                    uint4* __restrict__ dst, int E, int I, int rowbytes) {
+  const int chunks_per_row = rowbytes / 64;
+  const int npairs = (I / 16 + 1) / 2;
+  const size_t total = static_cast<size_t>(E) * npairs * chunks_per_row * 4 * 64;  // 16-B pieces
+  for (size_t c = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x; c < total;
+       c += static_cast<size_t>(gridDim.x) * blockDim.x) {
+    const int lane = static_cast<int>(c & 63);
+    const int f = static_cast<int>((c >> 6) & 3);
+    size_t q = c >> 8;
+    const int kc = static_cast<int>(q % chunks_per_row);
+    q /= chunks_per_row;
+    const int pair = static_cast<int>(q % npairs);
+    const int e = static_cast<int>(q / npairs);
+    const int row = (2 * pair + (f & 1)) * 16 + (lane & 15);
+    const uint4* src = (f >> 1) ? up : gate;
+    dst[c] = row < I ? src[((static_cast<size_t>(e) * I + row) * rowbytes + kc * 64 + (lane >> 4) * 16) / 16]
+                     : make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
 // A node's routing row, loaded once: experts e[j] and a bit per slot that
 // takes part in the dispatch.  A slot is skipped when its index lies outside
 // [0, E) or repeats the expert of an earlier slot of the same node (a repeated
@@ -294,10 +318,10 @@ __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f +
 // M-tile counts; per projection, the output tiles each wave computes on shared
 // A fragments (NTW) and the number of waves splitting a tile's K range (KS).
 #ifndef AMOE_KU_SMALL
-#define AMOE_KU_SMALL 2
+#define AMOE_KU_SMALL 1
 #endif
 #ifndef AMOE_KU_LARGE
-#define AMOE_KU_LARGE 2
+#define AMOE_KU_LARGE 1
 #endif
 #ifndef AMOE_GU_NTW
 #define AMOE_GU_NTW 2
@@ -346,32 +370,35 @@ constexpr int shared_a_pieces() {
   return 2 * best;
 }
 
-// acc[nb][mt] += sum over fragments kc in [kc0, kc1) of x[mt] (A, tokens) times
-// w[nb] (B, weight rows).  w[nb] / x[mt] point at this lane's 16-byte piece of
-// fragment 0; fragment kc sits kc*64 pieces (B) / kc*4 pieces (A) further.
-// Loads run two stages ahead of the MFMAs and carry no branches, so the only
-// waits are the in-order vmcnt waits on the stage being consumed.
+// acc[nb][mt] += sum over the K chunks c_i = c_first + i * c_step, 0 <= i < n,
+// of x[mt] (A, tokens) times w[nb] (B, weight rows).  w[nb] / x[mt] point at
+// this lane's 16-byte piece of chunk 0; chunk c sits c * wstride pieces (B) /
+// c * 4 pieces (A) further.  Loads run two stages ahead of the MFMAs and carry
+// no branches, so the only waits are the in-order vmcnt waits on the stage
+// being consumed.
 template <class P, int MT, int NB>
-__device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const uint4* const (&x)[MT],
-                                             int kc0, int kc1, floatx4 (&acc)[NB][MT]) {
+__device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const uint4* const (&x)[MT], int c_first,
+                                             int c_step, int n, int wstride, floatx4 (&acc)[NB][MT]) {
   constexpr int kU = Stage<MT>::kU;
   uint4 wb0[kU][NB], wb1[kU][NB], xb0[kU][MT], xb1[kU][MT];
-  auto load0 = [&](int c) {
+  auto load0 = [&](int i) {
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
+      const int c = c_first + (i + u) * c_step;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) wb0[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * kWave);
+      for (int nb = 0; nb < NB; ++nb) wb0[u][nb] = load_weight(w[nb] + static_cast<size_t>(c) * wstride);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) xb0[u][mt] = x[mt][(c + u) * 4];
+      for (int mt = 0; mt < MT; ++mt) xb0[u][mt] = x[mt][c * 4];
     }
   };
-  auto load1 = [&](int c) {
+  auto load1 = [&](int i) {
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
+      const int c = c_first + (i + u) * c_step;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) wb1[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * kWave);
+      for (int nb = 0; nb < NB; ++nb) wb1[u][nb] = load_weight(w[nb] + static_cast<size_t>(c) * wstride);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) xb1[u][mt] = x[mt][(c + u) * 4];
+      for (int mt = 0; mt < MT; ++mt) xb1[u][mt] = x[mt][c * 4];
     }
   };
   auto comp0 = [&]() {
@@ -393,30 +420,36 @@ __device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const 
   // Steady state without branches: the prefetch of the next stage is issued
   // unconditionally before the current stage is consumed, so the wait-count
   // pass sees straight-line code and only waits for the stage being used.
+  // The scheduling barriers keep the compiler from sinking a prefetch below
+  // the MFMAs of the stage before it (which would drain the pipeline: the
+  // waits for the current stage would then come before the next loads).
   // The last one or two stages are peeled off after the loop.
-  const int nst = (kc1 - kc0) / kU;
-  const int full_end = kc0 + nst * kU;
+  const int nst = n / kU;
   if (nst > 0) {
-    load0(kc0);
+    load0(0);
     int st = 0;
     for (; st + 2 < nst; st += 2) {
-      load1(kc0 + (st + 1) * kU);
+      load1((st + 1) * kU);
+      __builtin_amdgcn_sched_barrier(0);
       comp0();
-      load0(kc0 + (st + 2) * kU);
+      load0((st + 2) * kU);
+      __builtin_amdgcn_sched_barrier(0);
       comp1();
     }
     if (st + 1 < nst) {
-      load1(kc0 + (st + 1) * kU);
+      load1((st + 1) * kU);
+      __builtin_amdgcn_sched_barrier(0);
       comp0();
       comp1();
     } else {
       comp0();
     }
   }
-  for (int c = full_end; c < kc1; ++c) {
+  for (int i = nst * kU; i < n; ++i) {
+    const int c = c_first + i * c_step;
     uint4 wt[NB], xt[MT];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) wt[nb] = load_weight(w[nb] + static_cast<size_t>(c) * kWave);
+    for (int nb = 0; nb < NB; ++nb) wt[nb] = load_weight(w[nb] + static_cast<size_t>(c) * wstride);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) xt[mt] = x[mt][c * 4];
 #pragma unroll
@@ -433,7 +466,7 @@ __device__ __forceinline__ void stream_tiles(const uint4* const (&w)[NB], const 
 // 4 waves must call this with the same kc range (it contains barriers).
 template <class P, int MT, int NB>
 __device__ __forceinline__ void stream_tiles_shared(const uint4* const (&w)[NB], const uint4* const (&x)[MT],
-                                                    int KC, floatx4 (&acc)[NB][MT], uint4* xs) {
+                                                    int KC, int wstride, floatx4 (&acc)[NB][MT], uint4* xs) {
   constexpr int kU = Stage<MT>::kU;
   constexpr int kFr = kU * MT;                   // A fragments per stage
   constexpr int kMine = (kFr + 3) / 4;           // of which this wave loads
@@ -445,13 +478,13 @@ __device__ __forceinline__ void stream_tiles_shared(const uint4* const (&w)[NB],
 #pragma unroll
     for (int u = 0; u < kU; ++u)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) wb0[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * kWave);
+      for (int nb = 0; nb < NB; ++nb) wb0[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * wstride);
   };
   auto loadw1 = [&](int c) {
 #pragma unroll
     for (int u = 0; u < kU; ++u)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) wb1[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * kWave);
+      for (int nb = 0; nb < NB; ++nb) wb1[u][nb] = load_weight(w[nb] + static_cast<size_t>(c + u) * wstride);
   };
   // fragment f of a stage (step f / MT, M-tile f % MT) is loaded by wave f % 4;
   // every index below is a compile-time constant, the wave test is uniform
@@ -513,7 +546,7 @@ __device__ __forceinline__ void stream_tiles_shared(const uint4* const (&w)[NB],
   for (int c = nst * kU; c < KC; ++c) {
     uint4 wt[NB], xt[MT];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) wt[nb] = load_weight(w[nb] + static_cast<size_t>(c) * kWave);
+    for (int nb = 0; nb < NB; ++nb) wt[nb] = load_weight(w[nb] + static_cast<size_t>(c) * wstride);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) xt[mt] = x[mt][c * 4];
 #pragma unroll
@@ -527,11 +560,17 @@ __device__ __forceinline__ void stream_tiles_shared(const uint4* const (&w)[NB],
 // The two grouped projections share one pass structure.  A workgroup (4
 // waves) owns a run of 16-row output tiles of one active expert.  Each wave
 // computes NTW tiles that share its A fragments; the KS waves of a tile group
-// split the K range and add their partial tiles in LDS in a fixed order
-// (deterministic), so one workgroup covers 4 * NTW / KS tiles.
+// split the K chunks round-robin (wave s takes chunks s, s + KS, ...; the
+// group reads its weight run front to back together, which keeps the DRAM
+// accesses of the whole chip in far fewer open rows than per-wave K ranges)
+// and add their partial tiles in LDS in a fixed order (deterministic), so one
+// workgroup covers 4 * NTW / KS tiles.
 //   GateUp: rows of I, K = H, A = gathered hidden rows; each tile has a gate
 //           and an up fragment; SwiGLU -> act (bf16 for the bf16 path, fp32
-//           otherwise), written once per token row.
+//           otherwise), written once per token row.  NTW = 2: the gate and up
+//           fragments of a tile pair are adjacent in the packed layout
+//           ([E][I/32][K chunk][gate 2p, gate 2p+1, up 2p, up 2p+1]), so a
+//           K chunk of the pair is one 4 KiB run.
 //   Down:   rows of H, K = I, A = act rows of the expert; gate-scaled rows go
 //           to the token's slot row of ys.
 // ---------------------------------------------------------------------------
@@ -546,6 +585,7 @@ struct ProjShape {
 template <class P, Proj F, int MT, int NTW, int KS>
 __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* ent, int e, int tile_base, int n_e,
                                          int o_e, int m0, floatx4 (*red)[kWave][4], uint4* xs) {
+  static_assert(F != Proj::GateUp || NTW == 2, "the packed gate/up layout holds tile pairs");
   constexpr int NB = ProjShape<F, NTW, KS>::kNB;
   const int wave = wave_id(), lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
@@ -574,18 +614,26 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* 
       x[mt] = act + static_cast<size_t>(o_e + (m < n_e ? m : 0)) * rowq + g;
     }
   }
-  // tiles past the end are clamped to a valid tile: computed, never written
+  // tiles past the end are clamped to a valid tile (pair): computed, never written
   const uint4* w[NB];
+  int wstride;  // 16-byte pieces from one K chunk to the next
+  if (F == Proj::GateUp) {
+    const int npairs = (ntiles + 1) / 2;
+    const int pair = min(tile0 / 2, npairs - 1);
+    const uint4* base = static_cast<const uint4*>(p.w_gate_up) +
+                        (static_cast<size_t>(e) * npairs + pair) * KC * 4 * kWave + lane;
+    w[0] = base;              // gate, tile 2 pair
+    w[1] = base + 2 * kWave;  // up, tile 2 pair
+    w[2] = base + kWave;      // gate, tile 2 pair + 1
+    w[3] = base + 3 * kWave;  // up, tile 2 pair + 1
+    wstride = 4 * kWave;
+  } else {
 #pragma unroll
-  for (int j = 0; j < NTW; ++j) {
-    const int tile = min(tile0 + j, ntiles - 1);
-    const size_t frag0 = (static_cast<size_t>(e) * ntiles + tile) * KC;
-    if (F == Proj::GateUp) {
-      w[2 * j] = static_cast<const uint4*>(p.w_gate) + frag0 * kWave + lane;
-      w[2 * j + 1] = static_cast<const uint4*>(p.w_up) + frag0 * kWave + lane;
-    } else {
-      w[j] = static_cast<const uint4*>(p.w_down) + frag0 * kWave + lane;
+    for (int j = 0; j < NTW; ++j) {
+      const int tile = min(tile0 + j, ntiles - 1);
+      w[j] = static_cast<const uint4*>(p.w_down) + (static_cast<size_t>(e) * ntiles + tile) * KC * kWave + lane;
     }
+    wstride = kWave;
   }
   floatx4 acc[NB][MT];
 #pragma unroll
@@ -593,9 +641,9 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* 
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
   if constexpr (KS == 1)
-    stream_tiles_shared<P, MT, NB>(w, x, KC, acc, xs);
+    stream_tiles_shared<P, MT, NB>(w, x, KC, wstride, acc, xs);
   else
-    stream_tiles<P, MT, NB>(w, x, sub * KC / KS, (sub + 1) * KC / KS, acc);
+    stream_tiles<P, MT, NB>(w, x, sub, KS, (KC - sub + KS - 1) / KS, wstride, acc);
 
   if constexpr (KS > 1) {
     // fixed-order sum of the KS partial tiles, four fragments per LDS round
@@ -980,6 +1028,21 @@ hipError_t launch_down_col(const ForwardParams& p, const ColShape& c, hipStream_
 }
 
 }  // namespace
+
+size_t packed_gate_up_bytes(int is_bf16, int E, int I, int H) {
+  return static_cast<size_t>(E) * ((I / 16 + 1) / 2) * 32 * H * (is_bf16 ? 2 : 4) * 2;
+}
+
+hipError_t launch_pack_gate_up(const void* gate, const void* up, int is_bf16, int E, int I, int H, void* dst,
+                               hipStream_t stream) {
+  const size_t pieces = packed_gate_up_bytes(is_bf16, E, I, H) / 16;
+  const int block = 256;
+  const size_t want = (pieces + block - 1) / block;
+  const int grid = static_cast<int>(want < 65536 ? want : 65536);
+  pack_gate_up_kernel<<<grid, block, 0, stream>>>(static_cast<const uint4*>(gate), static_cast<const uint4*>(up),
+                                                  static_cast<uint4*>(dst), E, I, H * (is_bf16 ? 2 : 4));
+  return hipGetLastError();
+}
 
 hipError_t launch_pack(const void* src, int is_bf16, int E, int N, int K, void* dst, hipStream_t stream) {
   const int rowbytes = K * (is_bf16 ? 2 : 4);

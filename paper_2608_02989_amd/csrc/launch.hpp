@@ -50,11 +50,13 @@ hipError_t launch_select(const SelectParams& p, const TreeOffsets& offs, hipStre
 
 // ---- expert FFN (forward.hip) ----
 hipError_t launch_pack(const void* src, int is_bf16, int E, int N, int K, void* dst, hipStream_t stream);
+size_t packed_gate_up_bytes(int is_bf16, int E, int I, int H);
+hipError_t launch_pack_gate_up(const void* gate, const void* up, int is_bf16, int E, int I, int H, void* dst,
+                               hipStream_t stream);
 
 struct ForwardParams {
   const void* hidden;
-  const void* w_gate;
-  const void* w_up;
+  const void* w_gate_up;  // packed gate/up tile pairs
   const void* w_down;
   const int32_t* topk_idx;
   const float* topk_gate;

@@ -137,26 +137,53 @@ def pack_expert_weights(w: torch.Tensor, stream=None) -> torch.Tensor:
     return out
 
 
+class PackedGateUp:
+    """Gate and up stacks [E, I, H] packed together (acceptmoe_pack_gate_up_weights)."""
+
+    def __init__(self, data: torch.Tensor, E: int, I: int, H: int):
+        self.data, self.E, self.I, self.H = data, E, I, H
+        self.dtype = data.dtype
+
+
+def pack_gate_up_weights(w_gate: torch.Tensor, w_up: torch.Tensor, stream=None) -> PackedGateUp:
+    """Gate and up [E, I, H] stacks -> one PackedGateUp buffer (tile pairs, gate/up adjacent)."""
+    _need(w_gate, "w_gate", dim=3)
+    _need(w_up, "w_up", w_gate.dtype, 3)
+    if w_up.shape != w_gate.shape:
+        raise ValueError("w_gate and w_up must have the same shape [E, I, H]")
+    E, I, H = w_gate.shape
+    code = _dtype_code(w_gate)
+    n = int(lib().acceptmoe_packed_gate_up_bytes(code, E, I, H))
+    if n == 0:
+        raise ValueError(f"unsupported gate/up shape {tuple(w_gate.shape)}")
+    data = torch.empty(n // w_gate.element_size(), dtype=w_gate.dtype, device=w_gate.device)
+    check(lib().acceptmoe_pack_gate_up_weights(_ptr(w_gate), _ptr(w_up), code, E, I, H, _ptr(data),
+                                               _stream_ptr(stream)))
+    return PackedGateUp(data, E, I, H)
+
+
 def forward_workspace(T: int, H: int, I: int, E: int, k: int, dtype: torch.dtype, device) -> torch.Tensor:
     code = L.BF16 if dtype == torch.bfloat16 else L.F32
     n = lib().acceptmoe_moe_forward_workspace_size(T, H, I, E, k, code)
     return torch.empty(max(int(n), 256), dtype=torch.uint8, device=device)
 
 
-def moe_forward(hidden: torch.Tensor, w_gate_p: torch.Tensor, w_up_p: torch.Tensor, w_down_p: torch.Tensor,
+def moe_forward(hidden: torch.Tensor, w_gate_up: PackedGateUp, w_down_p: torch.Tensor,
                 topk_idx: torch.Tensor, topk_gate: torch.Tensor, out: torch.Tensor | None = None,
                 workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """Grouped SwiGLU expert FFN over packed weights (acceptmoe_moe_forward) -> [T, H] fp32."""
     _need(hidden, "hidden", dim=2)
-    for n_, w in (("w_gate", w_gate_p), ("w_up", w_up_p), ("w_down", w_down_p)):
-        _need(w, n_, hidden.dtype, 3)
+    if not isinstance(w_gate_up, PackedGateUp):
+        raise TypeError("w_gate_up must come from pack_gate_up_weights")
+    _need(w_gate_up.data, "w_gate_up", hidden.dtype, 1)
+    _need(w_down_p, "w_down", hidden.dtype, 3)
     _need(topk_idx, "topk_idx", torch.int32, 2)
     _need(topk_gate, "topk_gate", torch.float32, 2)
     T, H = hidden.shape
-    E, I, H2 = w_gate_p.shape
+    E, I = w_gate_up.E, w_gate_up.I
     k = topk_idx.shape[1]
-    if H2 != H or tuple(w_up_p.shape) != (E, I, H) or tuple(w_down_p.shape) != (E, H, I):
-        raise ValueError("weight stacks must be gate/up [E, I, H] and down [E, H, I]")
+    if w_gate_up.H != H or tuple(w_down_p.shape) != (E, H, I):
+        raise ValueError("weights must be gate/up packed from [E, I, H] stacks and down [E, H, I]")
     if tuple(topk_idx.shape) != (T, k) or tuple(topk_gate.shape) != (T, k):
         raise ValueError("topk_idx / topk_gate must be [T, k]")
     if out is None:
@@ -164,7 +191,7 @@ def moe_forward(hidden: torch.Tensor, w_gate_p: torch.Tensor, w_up_p: torch.Tens
     if workspace is None:
         workspace = forward_workspace(T, H, I, E, k, hidden.dtype, hidden.device)
     check(lib().acceptmoe_moe_forward(
-        _ptr(hidden), _dtype_code(hidden), _ptr(w_gate_p), _ptr(w_up_p), _ptr(w_down_p), T, H, I, E, k,
+        _ptr(hidden), _dtype_code(hidden), _ptr(w_gate_up.data), _ptr(w_down_p), T, H, I, E, k,
         _ptr(topk_idx), _ptr(topk_gate), _ptr(out), _ptr(workspace), workspace.numel(), _stream_ptr(stream)))
     return out
 
@@ -179,19 +206,14 @@ class VerifyLayer:
 
     def __init__(self, router_w: torch.Tensor, w_gate: torch.Tensor, w_up: torch.Tensor,
                  w_down: torch.Tensor, k: int, max_tokens: int, max_trees: int = 1, beta: float = 0.5,
-                 mode: int = L.MODE_SELF_SIZING, budget: int = 0, removal_cap: int = -1,
-                 packed: bool = False):
+                 mode: int = L.MODE_SELF_SIZING, budget: int = 0, removal_cap: int = -1):
         self.router_w = router_w  # [E, H] fp32, kept for reference checks
         self.router = pack_router_weights(router_w)
         self.E, self.I, self.H = w_gate.shape
         self.k, self.beta, self.mode, self.budget, self.removal_cap = k, beta, mode, budget, removal_cap
         self.dtype = w_gate.dtype
-        if packed:
-            self.wg, self.wu, self.wd = w_gate, w_up, w_down
-        else:
-            self.wg = pack_expert_weights(w_gate)
-            self.wu = pack_expert_weights(w_up)
-            self.wd = pack_expert_weights(w_down)
+        self.wgu = pack_gate_up_weights(w_gate, w_up)
+        self.wd = pack_expert_weights(w_down)
         dev = w_gate.device
         T = max_tokens
         self.logits = torch.empty((T, self.E), dtype=torch.float32, device=dev)
@@ -215,6 +237,6 @@ class VerifyLayer:
         select(logits, parent, depth, prob, tree_offsets, self.k, self.beta, self.mode, self.budget,
                self.removal_cap, resident, workspace=self.sel_ws, outputs=outs, stream=stream)
         out = self.out[:T]
-        moe_forward(hidden, self.wg, self.wu, self.wd, outs["idx"], outs["gate"], out=out,
+        moe_forward(hidden, self.wgu, self.wd, outs["idx"], outs["gate"], out=out,
                     workspace=self.fwd_ws, stream=stream)
         return logits, outs, out

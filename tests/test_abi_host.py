@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_error_string():
-    assert L.lib().acceptmoe_version() == 100
+    assert L.lib().acceptmoe_version() == 200
     assert isinstance(L.lib().acceptmoe_last_error(), bytes)
 
 
@@ -136,11 +136,29 @@ def test_pack_rejects():
     assert f(FAKE, L.BF16, 0, 32, 64, V(0x900000), None) == L.ERR_INVALID_ARG
 
 
+def test_pack_gate_up_sizes_and_rejects():
+    lib = L.lib()
+    sz = lib.acceptmoe_packed_gate_up_bytes
+    assert sz(L.BF16, 128, 768, 2048) == 2 * 128 * 768 * 2048 * 2        # I % 32 == 0: the two stacks
+    assert sz(L.F32, 3, 80, 64) == 3 * 96 * 64 * 4 * 2                   # I/16 odd: padded to 96 rows
+    assert sz(9, 3, 80, 64) == 0 and sz(L.F32, 0, 80, 64) == 0
+    f = lib.acceptmoe_pack_gate_up_weights
+    D = V(0x900000)
+    assert f(FAKE, FAKE, L.BF16, 2, 24, 64, D, None) == L.ERR_UNSUPPORTED         # I % 16
+    assert f(FAKE, FAKE, L.BF16, 2, 32, 48, D, None) == L.ERR_UNSUPPORTED         # H % 32
+    assert f(FAKE, FAKE, L.F32, 2, 32, 40, D, None) == L.ERR_UNSUPPORTED          # H % 16
+    assert f(FAKE, FAKE, 3, 2, 32, 64, D, None) == L.ERR_INVALID_ARG
+    assert f(FAKE, None, L.BF16, 2, 32, 64, D, None) == L.ERR_INVALID_ARG
+    assert f(FAKE, FAKE, L.BF16, 2, 32, 64, V(0x900008), None) == L.ERR_INVALID_ARG  # misaligned dst
+    assert f(FAKE, V(0x900000 + 4096), L.BF16, 2, 32, 64, D, None) == L.ERR_INVALID_ARG  # up overlaps dst
+    assert f(FAKE, FAKE, L.BF16, 0, 32, 64, D, None) == L.ERR_INVALID_ARG
+
+
 def fwd(**kw):
-    a = dict(h=FAKE, dt=L.BF16, wg=FAKE, wu=FAKE, wd=FAKE, T=8, H=256, I=128, E=16, k=2, idx=FAKE,
+    a = dict(h=FAKE, dt=L.BF16, wgu=FAKE, wd=FAKE, T=8, H=256, I=128, E=16, k=2, idx=FAKE,
              gate=FAKE, out=FAKE, ws=None, wsb=0)
     a.update(kw)
-    return L.lib().acceptmoe_moe_forward(a["h"], a["dt"], a["wg"], a["wu"], a["wd"], a["T"], a["H"], a["I"],
+    return L.lib().acceptmoe_moe_forward(a["h"], a["dt"], a["wgu"], a["wd"], a["T"], a["H"], a["I"],
                                          a["E"], a["k"], a["idx"], a["gate"], a["out"], a["ws"], a["wsb"],
                                          None)
 
@@ -154,6 +172,7 @@ def test_forward_rejects():
     assert fwd(k=40) == L.ERR_UNSUPPORTED
     assert fwd(T=-1) == L.ERR_INVALID_ARG
     assert fwd(out=None) == L.ERR_INVALID_ARG
+    assert fwd(wgu=None) == L.ERR_INVALID_ARG
     assert fwd(h=V(0x100008)) == L.ERR_INVALID_ARG         # misaligned
     assert fwd() == L.ERR_WORKSPACE
     assert fwd(T=0, h=None, out=None) == L.OK

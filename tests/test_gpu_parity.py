@@ -232,8 +232,8 @@ def test_select_parity_batch_with_invalid_trees(gpu, sizes):
 def forward_case(cfg, idx, gate, blk_hidden, layer=0, E=None):
     hdev, h64 = hidden_for(cfg, blk_hidden)
     wg, wu, wd = W.expert_weights_torch(cfg, layer, DEV, E=E)
-    got = ops.moe_forward(to_dev_hidden(cfg, hdev), ops.pack_expert_weights(wg), ops.pack_expert_weights(wu),
-                          ops.pack_expert_weights(wd), i32(idx), f32(gate))
+    got = ops.moe_forward(to_dev_hidden(cfg, hdev), ops.pack_gate_up_weights(wg, wu), ops.pack_expert_weights(wd),
+                          i32(idx), f32(gate))
     torch.cuda.synchronize()
     return got.cpu().numpy(), h64, (HostExperts(wg), HostExperts(wu), HostExperts(wd))
 
@@ -308,6 +308,47 @@ def test_forward_parity_path_limits(gpu, T, k, E, dtype):
     ref = O.moe_forward_grouped(h64, wg, wu, wd, idx, gate, cfg.dtype)
     err = normwise_rel(got, ref)
     assert err <= FWD_TOL[cfg.dtype], err
+
+
+# fp32 with I / 16 odd: the last gate/up tile pair is half padding (column-tile and per-slot paths)
+@pytest.mark.parametrize("T", [37, 300])
+def test_forward_parity_odd_tile_count(gpu, T):
+    cfg = W.LayerConfig("oddtiles", 97 + T, "f32", T=T, B=1, H=128, E=12, k=3, I=80, depth_max=6,
+                        commit_rule="depth_sibling", hidden_std=1.0)
+    rng = np.random.default_rng(T + 5)
+    h32 = rng.standard_normal((T, cfg.H)).astype(np.float32)
+    idx = np.stack([rng.permutation(cfg.E)[:cfg.k] for _ in range(T)]).astype(np.int32)
+    gate = rng.random((T, cfg.k)).astype(np.float32)
+    say(f"forward odd tile count T={T} I={cfg.I}")
+    got, h64, (wg, wu, wd) = forward_case(cfg, idx, gate, h32)
+    ref = O.moe_forward_grouped(h64, wg, wu, wd, idx, gate, cfg.dtype)
+    err = normwise_rel(got, ref)
+    assert err <= FWD_TOL[cfg.dtype], err
+
+
+def test_pack_gate_up_layout_documented(gpu):
+    # fp32 stacks whose values encode (matrix, e, i, h); I / 16 = 3 -> the last pair's second tiles are zero
+    E, I, H = 2, 48, 32
+    e_, i_, h_ = np.meshgrid(np.arange(E), np.arange(I), np.arange(H), indexing="ij")
+    g = (e_ * 1e6 + i_ * 1e3 + h_ + 1).astype(np.float32)
+    u = -g
+    pk = ops.pack_gate_up_weights(f32(g), f32(u))
+    nbytes = L.lib().acceptmoe_packed_gate_up_bytes(L.F32, E, I, H)
+    assert pk.data.numel() * 4 == nbytes == E * 2 * 32 * H * 4 * 2
+    frags = pk.data.cpu().numpy().reshape(-1, 64, 4)          # [fragment][lane][4 floats]
+    npairs, kc_per_row = 2, H * 4 // 64
+    assert frags.shape[0] == E * npairs * kc_per_row * 4
+    for fi in range(frags.shape[0]):
+        f = fi % 4
+        kc = (fi // 4) % kc_per_row
+        pair = (fi // 4 // kc_per_row) % npairs
+        e = fi // 4 // kc_per_row // npairs
+        src = u if f >= 2 else g
+        for lane in range(64):
+            row = (2 * pair + (f & 1)) * 16 + lane % 16
+            col = kc * 16 + (lane // 16) * 4
+            want = src[e, row, col:col + 4] if row < I else np.zeros(4, np.float32)
+            assert np.array_equal(frags[fi, lane], want), (fi, lane)
 
 
 def test_pack_router_layout_documented(gpu):
