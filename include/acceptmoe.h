@@ -247,6 +247,95 @@ int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_g
                               const float* topk_gate, float* out, void* workspace,
                               size_t workspace_bytes, void* stream);
 
+/*
+ * ---------------------------------------------------------------------------
+ * Physical expert offload (Sec. 3.4, offload paragraph; Sec. 4, offload setup)
+ * ---------------------------------------------------------------------------
+ * Each MoE layer keeps an X-slot expert pool in device memory and the packed
+ * weights of all E experts in pinned host memory.  The pool limits residency,
+ * not eligibility: selection sees the resident set as `resident_mask`, and an
+ * expert that receives a token while not resident is copied into a slot
+ * before the forward runs.  A block whose routed union exceeds X is served in
+ * waves of tokens whose unions fit.  The pool state is host memory owned by
+ * the caller; one state per layer; calls on one state must not overlap.
+ *
+ * Policy (the paper leaves these open; each is stated here):
+ *   - a slot holds one expert's gate, up and down weights of the layer;
+ *   - waves: tokens in node order join the current wave unless its routed
+ *     union would exceed X, else they open the next wave (needs X >= k);
+ *   - recency is kept per wave: each expert a wave uses is stamped with the
+ *     wave's time; a load evicts the oldest slot whose expert the wave does
+ *     not use (empty slots first, lower slot index on equal stamps);
+ *   - a wave's experts are visited in ascending index; one access per (wave,
+ *     expert), a hit when the expert is resident before the wave's loads.
+ *
+ * stats: int64[ACCEPTMOE_POOL_NUM_STATS], accumulated (never reset) by
+ * acceptmoe_pool_serve_wave.
+ */
+#define ACCEPTMOE_POOL_WAVES 0     /* waves served                                 */
+#define ACCEPTMOE_POOL_ACCESSES 1  /* (wave, routed expert) accesses               */
+#define ACCEPTMOE_POOL_HITS 2      /* accesses that found the expert resident      */
+#define ACCEPTMOE_POOL_MISSES 3    /* accesses that loaded the expert              */
+#define ACCEPTMOE_POOL_H2D_BYTES 4 /* bytes copied host -> device by those loads   */
+#define ACCEPTMOE_POOL_NUM_STATS 5
+
+/*
+ * acceptmoe_pool_state_bytes -- host bytes of the state of an X-slot pool over
+ * E experts (0 for X < 1 or E outside [1, ACCEPTMOE_MAX_EXPERTS]).
+ * acceptmoe_pool_init -- initialises `state` (8-byte aligned host memory of at
+ * least that size) to an empty pool.
+ */
+size_t acceptmoe_pool_state_bytes(int32_t X, int32_t E);
+int32_t acceptmoe_pool_init(void* state, size_t state_bytes, int32_t X, int32_t E);
+
+/*
+ * acceptmoe_pool_resident_mask -- mask[e] = 1 if expert e is in the pool, else
+ * 0 (host array of E bytes): the residency mask for the next block's
+ * selection (Eq. 7).
+ */
+int32_t acceptmoe_pool_resident_mask(const void* state, uint8_t* mask);
+
+/*
+ * acceptmoe_pool_plan_waves -- partitions the T tokens of a block into waves
+ * (policy above).  topk_idx: host [T, k] routing rows (entries outside
+ * [0, E) and repeats within a row are ignored); wave_of: host [T] output;
+ * n_waves: host output (0 when T == 0).  ACCEPTMOE_ERR_UNSUPPORTED when a
+ * single token routes to more than X experts.
+ */
+int32_t acceptmoe_pool_plan_waves(const int32_t* topk_idx, int32_t T, int32_t k, int32_t E,
+                                  int32_t X, int32_t* wave_of, int32_t* n_waves);
+
+/*
+ * acceptmoe_pool_serve_wave -- makes every expert routed by the tokens of wave
+ * `wave` resident (hits refresh recency; misses evict and load), then writes
+ * slot_idx (host [T, k]): the slot of each entry's expert for the wave's
+ * tokens, -1 for other tokens and for ignored entries, so that
+ * acceptmoe_moe_forward over the pool (E = X experts, gates unchanged) runs
+ * that wave.
+ *   host_gate_up, host_down  pinned host stacks of all E experts in the
+ *                            acceptmoe_pack_gate_up_weights /
+ *                            acceptmoe_pack_expert_weights layouts
+ *   pool_gate_up, pool_down  device pools of X slots in the same layouts
+ *   gate_up_bytes, down_bytes bytes of one expert in each stack
+ * Loads are hipMemcpyAsync on `stream` (stream-ordered before any later
+ * launch on it).  With all four weight pointers NULL only the bookkeeping is
+ * done (planning and traffic accounting without copies).
+ */
+int32_t acceptmoe_pool_serve_wave(void* state, const int32_t* topk_idx, const int32_t* wave_of,
+                                  int32_t wave, int32_t T, int32_t k, const void* host_gate_up,
+                                  const void* host_down, void* pool_gate_up, void* pool_down,
+                                  size_t gate_up_bytes, size_t down_bytes, int32_t* slot_idx,
+                                  int64_t* stats, void* stream);
+
+/*
+ * acceptmoe_copy_rows -- dst[t, :] = src[t, :] (fp32 [T, H] device arrays)
+ * for every t with row_tag[t] == tag (device int32 [T]); other rows of dst
+ * are left as they are.  Joins the outputs of a block served in waves.
+ * Requires H % 4 == 0, T <= 65535, 16-byte aligned src and dst.
+ */
+int32_t acceptmoe_copy_rows(const float* src, float* dst, const int32_t* row_tag, int32_t tag,
+                            int32_t T, int32_t H, void* stream);
+
 /* Thread-local description of the last error (empty string if none). */
 const char* acceptmoe_last_error(void);
 

@@ -26,6 +26,10 @@ MODE_MOESPEC = 3
 MODE_COUNT = 4
 
 NUM_STATS = 10
+
+# offload pool counters (int64[POOL_NUM_STATS], accumulated by acceptmoe_pool_serve_wave)
+POOL_WAVES, POOL_ACCESSES, POOL_HITS, POOL_MISSES, POOL_H2D_BYTES = range(5)
+POOL_NUM_STATS = 5
 MAX_EXPERTS = 512
 MAX_TOPK = 32
 MAX_TREES = 256
@@ -50,6 +54,13 @@ SIGNATURES = {
     "acceptmoe_pack_gate_up_weights": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp]),
     "acceptmoe_moe_forward": (_i32, [_vp, _i32, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp,
                                      _vp, _vp, _sz, _vp]),
+    "acceptmoe_pool_state_bytes": (_sz, [_i32, _i32]),
+    "acceptmoe_pool_init": (_i32, [_vp, _sz, _i32, _i32]),
+    "acceptmoe_pool_resident_mask": (_i32, [_vp, _vp]),
+    "acceptmoe_pool_plan_waves": (_i32, [_vp, _i32, _i32, _i32, _i32, _vp, _vp]),
+    "acceptmoe_pool_serve_wave": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _sz, _vp, _vp,
+                                         _vp]),
+    "acceptmoe_copy_rows": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _vp]),
     "acceptmoe_last_error": (ctypes.c_char_p, []),
     "acceptmoe_version": (_i32, []),
 }

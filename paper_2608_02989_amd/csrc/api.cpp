@@ -9,35 +9,19 @@
 #include <cstdio>
 #include <cstring>
 
+#include "abi_util.hpp"
 #include "launch.hpp"
 
-namespace {
-
-thread_local char g_err[512] = "";
-
-int fail(int code, const char* fmt, ...) {
-  va_list ap;
-  va_start(ap, fmt);
-  std::vsnprintf(g_err, sizeof g_err, fmt, ap);
-  va_end(ap);
-  return code;
-}
-
-void clear_err() { g_err[0] = '\0'; }
-
-bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
-
-int hip_fail(hipError_t e, const char* what) {
-  return fail(ACCEPTMOE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
-}
-
-}  // namespace
+using amoe::abi::aligned;
+using amoe::abi::clear_err;
+using amoe::abi::fail;
+using amoe::abi::hip_fail;
 
 extern "C" {
 
-const char* acceptmoe_last_error(void) { return g_err; }
+const char* acceptmoe_last_error(void) { return amoe::abi::g_err; }
 
-int32_t acceptmoe_version(void) { return 200; }
+int32_t acceptmoe_version(void) { return 300; }
 
 // ---------------------------------------------------------------------------
 size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H) {

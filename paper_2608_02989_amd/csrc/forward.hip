@@ -1027,7 +1027,25 @@ hipError_t launch_down_col(const ForwardParams& p, const ColShape& c, hipStream_
   return c.nb == 2 ? launch_down_col_nb<P, 2>(p, c, stream) : launch_down_col_nb<P, 1>(p, c, stream);
 }
 
+// dst[t, :] = src[t, :] for the rows whose tag equals `tag` (float4 columns)
+__global__ void copy_rows_kernel(const float4* __restrict__ src, float4* __restrict__ dst,
+                                 const int32_t* __restrict__ row_tag, int tag, int T, int H4) {
+  const int t = blockIdx.y;
+  if (t >= T || row_tag[t] != tag) return;
+  for (int c = blockIdx.x * blockDim.x + threadIdx.x; c < H4; c += gridDim.x * blockDim.x)
+    dst[static_cast<size_t>(t) * H4 + c] = src[static_cast<size_t>(t) * H4 + c];
+}
+
 }  // namespace
+
+hipError_t launch_copy_rows(const float* src, float* dst, const int32_t* row_tag, int tag, int T, int H,
+                            hipStream_t stream) {
+  if (H % 4 != 0) return hipErrorInvalidValue;
+  const int H4 = H / 4;
+  copy_rows_kernel<<<dim3((H4 + 255) / 256, T), 256, 0, stream>>>(reinterpret_cast<const float4*>(src),
+                                                                 reinterpret_cast<float4*>(dst), row_tag, tag, T, H4);
+  return hipGetLastError();
+}
 
 size_t packed_gate_up_bytes(int is_bf16, int E, int I, int H) {
   return static_cast<size_t>(E) * ((I / 16 + 1) / 2) * 32 * H * (is_bf16 ? 2 : 4) * 2;

@@ -240,3 +240,149 @@ class VerifyLayer:
         moe_forward(hidden, self.wgu, self.wd, outs["idx"], outs["gate"], out=out,
                     workspace=self.fwd_ws, stream=stream)
         return logits, outs, out
+
+
+# ---------------------------------------------------------------------------
+# physical expert offload (acceptmoe_pool_*, acceptmoe_copy_rows)
+# ---------------------------------------------------------------------------
+def _host_ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+class OffloadPool:
+    """X-slot expert pool of one layer: LRU state in host memory (the library's),
+    X packed expert slots in device memory, and the layer's E packed experts in
+    pinned host memory.  Built without weights it keeps only the books (routing
+    to slots, hits, misses, host-to-device bytes) and copies nothing."""
+
+    def __init__(self, X: int, E: int, w_gate: torch.Tensor | None = None, w_up: torch.Tensor | None = None,
+                 w_down: torch.Tensor | None = None, expert_bytes: int = 0):
+        n = int(lib().acceptmoe_pool_state_bytes(X, E))
+        if n == 0:
+            raise ValueError(f"unsupported pool X={X} E={E}")
+        self._state = np.zeros((n + 7) // 8, np.int64)  # 8-byte aligned
+        check(lib().acceptmoe_pool_init(_host_ptr(self._state), n, X, E))
+        self.X, self.E = X, E
+        self.stats = np.zeros(L.POOL_NUM_STATS, np.int64)
+        self.physical = w_gate is not None
+        self.gu_bytes, self.dn_bytes = 0, 0
+        if self.physical:
+            gu = pack_gate_up_weights(w_gate, w_up)
+            dn = pack_expert_weights(w_down)
+            torch.cuda.synchronize()
+            self.dtype, self.I, self.H = w_gate.dtype, w_gate.shape[1], w_gate.shape[2]
+            gub = gu.data.view(torch.uint8)
+            dnb = dn.view(torch.uint8).reshape(-1)
+            self.gu_bytes, self.dn_bytes = gub.numel() // E, dnb.numel() // E
+            # the full stacks live in pinned host memory; the device copies are dropped
+            self.host_gu = torch.empty(gub.numel(), dtype=torch.uint8, pin_memory=True)
+            self.host_dn = torch.empty(dnb.numel(), dtype=torch.uint8, pin_memory=True)
+            self.host_gu.copy_(gub)
+            self.host_dn.copy_(dnb)
+            del gu, dn, gub, dnb
+            dev = w_gate.device
+            self.pool_gu = torch.empty(X * self.gu_bytes, dtype=torch.uint8, device=dev)
+            self.pool_dn = torch.empty(X * self.dn_bytes, dtype=torch.uint8, device=dev)
+            self.gate_up = PackedGateUp(self.pool_gu.view(self.dtype), X, self.I, self.H)
+            self.down = self.pool_dn.view(self.dtype).view(X, self.H, self.I)
+        self.expert_bytes = (self.gu_bytes + self.dn_bytes) if self.physical else int(expert_bytes)
+
+    def resident_mask(self) -> np.ndarray:
+        m = np.zeros(self.E, np.uint8)
+        check(lib().acceptmoe_pool_resident_mask(_host_ptr(self._state), _host_ptr(m)))
+        return m
+
+    def plan_waves(self, idx: np.ndarray):
+        idx = np.ascontiguousarray(idx, np.int32)
+        T, k = idx.shape
+        wave_of = np.zeros(max(T, 1), np.int32)
+        n = ctypes.c_int32(0)
+        check(lib().acceptmoe_pool_plan_waves(_host_ptr(idx), T, k, self.E, self.X, _host_ptr(wave_of),
+                                              ctypes.byref(n)))
+        return wave_of[:T], int(n.value)
+
+    def serve_wave(self, idx: np.ndarray, wave_of: np.ndarray, wave: int, stream=None) -> np.ndarray:
+        """Loads the wave's missing experts (stream-ordered) and returns its routing rewritten to slots."""
+        idx = np.ascontiguousarray(idx, np.int32)
+        wave_of = np.ascontiguousarray(wave_of, np.int32)
+        T, k = idx.shape
+        slot = np.full((max(T, 1), k), -1, np.int32)
+        if self.physical:
+            ptrs = (_ptr(self.host_gu), _ptr(self.host_dn), _ptr(self.pool_gu), _ptr(self.pool_dn))
+            gub, dnb, s = self.gu_bytes, self.dn_bytes, _stream_ptr(stream)
+        else:
+            ptrs = (ctypes.c_void_p(0),) * 4
+            gub, dnb, s = self.expert_bytes, 0, ctypes.c_void_p(0)
+        check(lib().acceptmoe_pool_serve_wave(_host_ptr(self._state), _host_ptr(idx), _host_ptr(wave_of), wave, T, k,
+                                              *ptrs, gub, dnb, _host_ptr(slot), _host_ptr(self.stats), s))
+        return slot[:T]
+
+
+def copy_rows(src: torch.Tensor, dst: torch.Tensor, row_tag: torch.Tensor, tag: int, stream=None):
+    """dst[t] = src[t] where row_tag[t] == tag (acceptmoe_copy_rows)."""
+    _need(src, "src", torch.float32, 2)
+    _need(dst, "dst", torch.float32, 2)
+    _need(row_tag, "row_tag", torch.int32, 1)
+    T, H = src.shape
+    if tuple(dst.shape) != (T, H) or row_tag.shape[0] != T:
+        raise ValueError("copy_rows: shapes must match")
+    check(lib().acceptmoe_copy_rows(_ptr(src), _ptr(dst), _ptr(row_tag), int(tag), T, H, _stream_ptr(stream)))
+
+
+class OffloadLayer:
+    """One MoE layer served from an X-slot pool (Sec. 3.4 offload paragraph).
+
+    step(): route -> select with the pool's resident set as mask -> routing
+    copied to the host -> waves planned -> per wave: missing experts loaded
+    into slots, routing rewritten to slots, forward over the pool (E = X) ->
+    wave outputs joined.  The host round trip after selection is the
+    synchronous decision point of the offload path."""
+
+    def __init__(self, router_w: torch.Tensor, w_gate: torch.Tensor, w_up: torch.Tensor, w_down: torch.Tensor,
+                 k: int, X: int, max_tokens: int, beta: float = 0.5, mode: int = L.MODE_SELF_SIZING,
+                 budget: int = 0, removal_cap: int = -1):
+        self.router = pack_router_weights(router_w)
+        self.E, self.I, self.H = w_gate.shape
+        self.k, self.X, self.beta, self.mode, self.budget, self.removal_cap = k, X, beta, mode, budget, removal_cap
+        self.pool = OffloadPool(X, self.E, w_gate, w_up, w_down)
+        dev = w_gate.device
+        T = max_tokens
+        self.logits = torch.empty((T, self.E), dtype=torch.float32, device=dev)
+        self.sel_ws = select_workspace(T, self.E, k, dev)
+        self.sel_out = {
+            "eligible": torch.empty((1, self.E), dtype=torch.uint8, device=dev),
+            "idx": torch.empty((T, k), dtype=torch.int32, device=dev),
+            "gate": torch.empty((T, k), dtype=torch.float32, device=dev),
+            "stats": torch.empty((1, L.NUM_STATS), dtype=torch.int32, device=dev),
+        }
+        self.mask = torch.empty(self.E, dtype=torch.uint8, device=dev)
+        self.slot_idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+        self.wave_tag = torch.empty(T, dtype=torch.int32, device=dev)
+        self.fwd_ws = forward_workspace(T, self.H, self.I, X, k, w_gate.dtype, dev)
+        self.out = torch.empty((T, self.H), dtype=torch.float32, device=dev)
+        self.out_wave = torch.empty((T, self.H), dtype=torch.float32, device=dev)
+
+    def step(self, hidden, parent, depth, prob):
+        """One block (one tree) through the layer on the current stream; returns (outs, out, wave_of)."""
+        T = hidden.shape[0]
+        logits = self.logits[:T]
+        route(hidden, self.router, out=logits)
+        self.mask.copy_(torch.from_numpy(self.pool.resident_mask()))
+        outs = {"eligible": self.sel_out["eligible"], "idx": self.sel_out["idx"][:T],
+                "gate": self.sel_out["gate"][:T], "stats": self.sel_out["stats"]}
+        select(logits, parent, depth, prob, None, self.k, self.beta, self.mode, self.budget, self.removal_cap,
+               self.mask, workspace=self.sel_ws, outputs=outs)
+        idx = outs["idx"].cpu().numpy()
+        wave_of, nw = self.pool.plan_waves(idx)
+        out = self.out[:T]
+        if nw > 1:
+            self.wave_tag[:T].copy_(torch.from_numpy(wave_of))
+        for w in range(nw):
+            slot = self.pool.serve_wave(idx, wave_of, w)
+            self.slot_idx[:T].copy_(torch.from_numpy(slot))
+            target = out if nw == 1 else self.out_wave[:T]
+            moe_forward(hidden, self.pool.gate_up, self.pool.down, self.slot_idx[:T], outs["gate"], out=target,
+                        workspace=self.fwd_ws)
+            if nw > 1:
+                copy_rows(target, out, self.wave_tag[:T], w)
+        return outs, out, wave_of
