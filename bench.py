@@ -44,6 +44,13 @@ def parse():
     ap.add_argument("--no-alt", action="store_true", help="skip the i.i.d. (rho = 0) companion run")
     ap.add_argument("--graph", type=int, default=1, help="time HIP-graph replays of the step sequence (1/0)")
     ap.add_argument("--stack-blocks", type=int, default=8, help="blocks timed through a whole layer stack")
+    ap.add_argument("--offload", action="store_true",
+                    help="expert-offload report (X-slot pools, LRU, waves) on a synthetic decode trace")
+    ap.add_argument("--pool-slots", type=int, default=48, help="X, expert slots per layer pool")
+    ap.add_argument("--trace-blocks", type=int, default=96, help="blocks of the offload trace")
+    ap.add_argument("--trace-warmup", type=int, default=16, help="leading trace blocks not counted")
+    ap.add_argument("--rho-step", type=float, default=0.9, help="root correlation of consecutive trace blocks")
+    ap.add_argument("--phys-layers", type=int, default=4, help="layers of the physical (copying) offload run")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="only run a plain device copy of MB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -96,6 +103,9 @@ def main():
     args = parse()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.offload:
+        offload_report(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this layer runs on a single MI355X "
@@ -404,6 +414,153 @@ def stack_report(args, cfg):
                    "stack_pass_us_per_layer": round(total_us / nb / nl, 2),
                    "stack_pass_weight_GBs": round(byts / (total_us * 1e-6) / 1e9, 1),
                    "timing": "eager launches, 48 distinct resident layers per block"})
+    print(json.dumps(report), flush=True)
+
+
+def offload_report(args):
+    """Physical expert offload on a synthetic decode trace (the traffic / hit-rate
+    comparison of Sec. 4, Table 2, on stand-in inputs).
+
+    Trace: the 48-layer Qwen3-30B-A3B stack shape (T = 60 draft trees, E = 128,
+    k = 8); consecutive blocks' root states are correlated (--rho-step), every
+    layer has its own router, hidden states and X-slot pool.  Methods, each on
+    fresh pools: Vanilla AR (one token per step, natural routing), Standard SD
+    (the whole draft tree, natural routing) and AcceptMoE (self-sized eligible
+    set pruned against the pool's resident set).  Part 1 (all layers): routing
+    on the GPU, pool bookkeeping without copies -> H2D MiB per block / per
+    token and hit rate after a warm-up.  Part 2 (--phys-layers): the same trace
+    with real pinned-host -> pool copies and the forward over the pool, timed.
+    Tokens per block: AR 1; tree methods sum over depths d of the largest
+    commitment probability at depth d (the chance the verified prefix reaches
+    depth d, root = 1): the expected committed length of the synthetic trees.
+    """
+    import torch
+
+    from paper_2608_02989_amd import _lib as L
+    from paper_2608_02989_amd import ops
+    from paper_2608_02989_amd import workload as W
+
+    t0 = time.time()
+
+    def log(msg):
+        print(f"[offload {time.time() - t0:6.1f}s] {msg}", file=sys.stderr, flush=True)
+
+    dev = "cuda"
+    cfg = W.CONFIGS["qwen3_30b_a3b_x48"]
+    X, nb, warm = args.pool_slots, args.trace_blocks, args.trace_warmup
+    nl, T, E, k = cfg.layers, cfg.T, cfg.E, cfg.k
+    methods = [("vanilla_ar", L.MODE_ALL_EXPERTS, True), ("standard_sd", L.MODE_ALL_EXPERTS, False),
+               ("acceptmoe", L.MODE_SELF_SIZING, False)]
+    routers = [ops.pack_router_weights(torch.from_numpy(W.router_weights(cfg, l)).to(dev)) for l in range(nl)]
+    roots = [W.trace_roots(cfg, l, nb, args.rho_step) for l in range(nl)]
+    # inputs of every (block, layer), shared by the methods
+    inputs, tau = [], []
+    for b in range(nb):
+        per = []
+        for l in range(nl):
+            blk = W.make_block(cfg, block=b, layer=l, rho=args.rho, tree_layer=0, root=roots[l][b])
+            h = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(dev)
+            per.append((h,) + tuple(torch.from_numpy(a).to(dev) for a in (blk.parent, blk.depth, blk.prob)))
+        inputs.append(per)
+        pd = {}
+        for d_, p_ in zip(blk.depth.tolist(), blk.prob.astype(np.float64).tolist()):
+            pd[d_] = max(pd.get(d_, 0.0), p_)
+        tau.append(float(sum(pd.values())))
+        if b % 32 == 31:
+            log(f"{b + 1} trace blocks generated")
+    tau_tree = float(np.mean(tau[warm:]))
+    logits = torch.empty((T, E), dtype=torch.float32, device=dev)
+    ws = ops.select_workspace(T, E, k, dev)
+    mask_dev = torch.empty(E, dtype=torch.uint8, device=dev)
+    outs = {"eligible": torch.empty((1, E), dtype=torch.uint8, device=dev),
+            "idx": torch.empty((T, k), dtype=torch.int32, device=dev),
+            "gate": torch.empty((T, k), dtype=torch.float32, device=dev),
+            "stats": torch.empty((1, L.NUM_STATS), dtype=torch.int32, device=dev)}
+
+    def node_inputs(inp, single):
+        h, par, dep, prob = inp
+        return (h[:1], par[:1], dep[:1], prob[:1]) if single else inp
+
+    results = {}
+    for name, mode, single in methods:
+        pools = [ops.OffloadPool(X, E, expert_bytes=cfg.expert_bytes) for _ in range(nl)]
+        base = np.zeros(L.POOL_NUM_STATS, np.int64)
+        routed = []
+        for b in range(nb):
+            if b == warm:
+                base = sum(p.stats for p in pools)
+            for l in range(nl):
+                h, par, dep, prob = node_inputs(inputs[b][l], single)
+                Tb = h.shape[0]
+                ops.route(h, routers[l], out=logits[:Tb])
+                mask_dev.copy_(torch.from_numpy(pools[l].resident_mask()))
+                o = {"eligible": outs["eligible"], "idx": outs["idx"][:Tb], "gate": outs["gate"][:Tb],
+                     "stats": outs["stats"]}
+                ops.select(logits[:Tb], par, dep, prob, None, k, mode=mode, resident=mask_dev, workspace=ws,
+                           outputs=o)
+                idx = o["idx"].cpu().numpy()
+                wave_of, n = pools[l].plan_waves(idx)
+                for w in range(n):
+                    pools[l].serve_wave(idx, wave_of, w)
+                if b >= warm:
+                    routed.append(len(np.unique(idx[idx >= 0])))
+        st = sum(p.stats for p in pools) - base
+        blocks = nb - warm
+        tok = blocks * (1.0 if single else tau_tree)
+        mib = st[L.POOL_H2D_BYTES] / 2**20
+        results[name] = {"blocks": blocks, "tokens_per_block": round(1.0 if single else tau_tree, 3),
+                         "h2d_MiB_per_block": round(float(mib) / blocks, 1),
+                         "h2d_MiB_per_token": round(float(mib) / tok, 1),
+                         "hit_rate": round(float(st[L.POOL_HITS]) / max(1, int(st[L.POOL_ACCESSES])), 4),
+                         "loads_per_block_layer": round(float(st[L.POOL_MISSES]) / (blocks * nl), 2),
+                         "routed_per_block_layer": round(float(np.mean(routed)), 2),
+                         "waves_per_block_layer": round(float(st[L.POOL_WAVES]) / (blocks * nl), 3)}
+        log(f"{name}: {results[name]}")
+
+    # part 2: physical copies and the forward over the pools, timed (a few layers)
+    npl = min(args.phys_layers, nl)
+    phys_layers = []
+    for l in range(npl):
+        wg, wu, wd = W.expert_weights_torch(cfg, l, dev)
+        phys_layers.append((wg, wu, wd))
+    log(f"{npl} layers of weights generated")
+    for name, mode, single in methods:
+        layers = []
+        for l in range(npl):
+            wg, wu, wd = phys_layers[l]
+            layers.append(ops.OffloadLayer(torch.from_numpy(W.router_weights(cfg, l)).to(dev), wg, wu, wd, k, X,
+                                           max_tokens=T, mode=mode))
+        torch.cuda.synchronize()
+        base = np.zeros(L.POOL_NUM_STATS, np.int64)
+        for b in range(nb):
+            if b == warm:
+                torch.cuda.synchronize()
+                base = sum(ly.pool.stats for ly in layers)
+                t_start = time.perf_counter()
+            for l in range(npl):
+                layers[l].step(*node_inputs(inputs[b][l], single))
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t_start
+        st = sum(ly.pool.stats for ly in layers) - base
+        steps = (nb - warm) * npl
+        results[name].update({
+            "phys_layers": npl, "phys_us_per_block_layer": round(elapsed / steps * 1e6, 1),
+            "phys_us_per_token_layer": round(elapsed / steps * 1e6 / (1.0 if single else tau_tree), 1),
+            "phys_loads_per_block_layer": round(float(st[L.POOL_MISSES]) / steps, 2),
+            "phys_h2d_GBs": round(float(st[L.POOL_H2D_BYTES]) / elapsed / 1e9, 2)})
+        log(f"{name} physical: {results[name]}")
+        del layers
+        torch.cuda.empty_cache()
+    sd, am = results["standard_sd"], results["acceptmoe"]
+    report = {"report": "expert offload on a synthetic decode trace", "config": cfg.name, "X": X,
+              "layers": nl, "E": E, "k": k, "T": T, "rho_tree": args.rho, "rho_step": args.rho_step,
+              "trace_blocks": nb, "warmup_blocks": warm, "expert_MiB": round(cfg.expert_bytes / 2**20, 3),
+              "methods": results,
+              "acceptmoe_vs_sd": {
+                  "h2d_per_token_change_pct": round(100.0 * (am["h2d_MiB_per_token"] / sd["h2d_MiB_per_token"] - 1), 1),
+                  "hit_rate_change_pp": round(100.0 * (am["hit_rate"] - sd["hit_rate"]), 1)},
+              "timing": "wall clock of eager steps (route, select, host round trip, loads, forward)",
+              "data": "synthetic"}
     print(json.dumps(report), flush=True)
 
 

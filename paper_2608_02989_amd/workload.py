@@ -33,7 +33,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-STREAM_TREE, STREAM_HIDDEN, STREAM_ROUTER, STREAM_EXPERTS, STREAM_COMMIT, STREAM_MASK = range(6)
+STREAM_TREE, STREAM_HIDDEN, STREAM_ROUTER, STREAM_EXPERTS, STREAM_COMMIT, STREAM_MASK, STREAM_TRACE = range(7)
 
 
 @dataclass(frozen=True)
@@ -145,16 +145,38 @@ def commit_probs(rng: np.random.Generator, rule: str, depth, sib) -> np.ndarray:
     raise ValueError(rule)
 
 
-def correlated_hidden(rng: np.random.Generator, parent, H: int, std: float, rho: float) -> np.ndarray:
-    """fp32 hidden states along the tree: child = rho*parent + sqrt(1-rho^2)*eps."""
+def correlated_hidden(rng: np.random.Generator, parent, H: int, std: float, rho: float,
+                      root=None) -> np.ndarray:
+    """fp32 hidden states along the tree: child = rho*parent + sqrt(1-rho^2)*eps.
+
+    root: optional unit-variance state [H] for the root (default: a fresh draw)."""
     T = len(parent)
     h = np.empty((T, H), np.float64)
     c = np.sqrt(max(0.0, 1.0 - rho * rho))
     for t in range(T):
         eps = rng.standard_normal(H)
         p = int(parent[t])
-        h[t] = eps if p < 0 else rho * h[p] + c * eps
+        if p < 0:
+            h[t] = eps if root is None else root
+        else:
+            h[t] = rho * h[p] + c * eps
     return (h * std).astype(np.float32)
+
+
+def trace_roots(cfg: LayerConfig, layer: int, n_blocks: int, rho_step: float) -> np.ndarray:
+    """Unit-variance root states of consecutive blocks of a decode trace on one
+    layer: root_b = rho_step * root_{b-1} + sqrt(1 - rho_step^2) * eps_b, so
+    consecutive blocks route alike (the temporal locality an expert cache
+    feeds on); rho_step = 0 makes blocks independent."""
+    rng = rng_for(cfg.cfg_id, 0, layer, STREAM_TRACE)
+    c = np.sqrt(max(0.0, 1.0 - rho_step * rho_step))
+    out = np.empty((n_blocks, cfg.H), np.float64)
+    r = rng.standard_normal(cfg.H)
+    for b in range(n_blocks):
+        if b > 0:
+            r = rho_step * r + c * rng.standard_normal(cfg.H)
+        out[b] = r
+    return out
 
 
 # ---------------------------------------------------------------------------
@@ -172,12 +194,14 @@ class Block:
 
 
 def make_block(cfg: LayerConfig, block: int = 0, layer: int = 0, rho: float = 0.9,
-               T: int | None = None, B: int | None = None, tree_layer: int | None = None) -> Block:
+               T: int | None = None, B: int | None = None, tree_layer: int | None = None,
+               root=None) -> Block:
     """Trees, probabilities, hidden states (and mask) of one verification block.
 
     tree_layer selects the seed of the tree structure (default: layer); a
     block seen by every layer of a stack keeps one tree (tree_layer = 0) while
-    each layer draws its own hidden states.
+    each layer draws its own hidden states.  root: optional unit-variance root
+    state (one tree; see trace_roots).
     """
     T = cfg.T if T is None else T
     B = cfg.B if B is None else B
@@ -190,7 +214,7 @@ def make_block(cfg: LayerConfig, block: int = 0, layer: int = 0, rho: float = 0.
         pr = commit_probs(rng_for(cfg.cfg_id, block, tl * 1000 + b, STREAM_COMMIT),
                           cfg.commit_rule, dep, sib)
         hs = correlated_hidden(rng_for(cfg.cfg_id, block, layer * 1000 + b, STREAM_HIDDEN),
-                               par, cfg.H, cfg.hidden_std, rho)
+                               par, cfg.H, cfg.hidden_std, rho, root=root if b == 0 else None)
         base = offsets[-1]
         parents.append(np.where(par < 0, -1, par + base).astype(np.int32))
         depths.append(dep)
