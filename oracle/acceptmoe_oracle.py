@@ -174,6 +174,36 @@ def depth_counts(depth) -> dict:
     return counts
 
 
+def commit_counts(depth, on_path, D: int):
+    """Offline counts behind p_hat (Sec. 3.2): m_d = proposed nodes at draft
+    position d, c_d = those lying on the accepted output prefix.  Positions
+    outside [0, D) are not counted."""
+    m = np.zeros(D, np.int64)
+    c = np.zeros(D, np.int64)
+    for d, a in zip(depth, on_path):
+        d = int(d)
+        if 0 <= d < D:
+            m[d] += 1
+            c[d] += 1 if a else 0
+    return m, c
+
+
+def commit_estimate(m, c) -> np.ndarray:
+    """p_hat_d = c_d / m_d (Sec. 3.2), rounded once to fp32 (the precision the
+    selector takes); a position never observed (m_d = 0) gets 0."""
+    out = np.zeros(len(m), np.float32)
+    for d in range(len(m)):
+        out[d] = np.float32(c[d] / m[d]) if m[d] > 0 else np.float32(0.0)
+    return out
+
+
+def commit_expand(p_hat, depth) -> np.ndarray:
+    """Per-node commitment probabilities p_t = p_hat[d_t]; positions beyond the
+    table get 0 (never observed)."""
+    D = len(p_hat)
+    return np.array([p_hat[int(d)] if 0 <= int(d) < D else 0.0 for d in depth], np.float32)
+
+
 def importance(depth, prob, beta: float) -> np.ndarray:
     """alpha_t = p_{d_t}^beta * N_{d_t}^{-1/2}  (Sec. 3.2, Eq. 3)."""
     N = depth_counts(depth)

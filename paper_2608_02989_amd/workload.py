@@ -145,6 +145,39 @@ def commit_probs(rng: np.random.Generator, rule: str, depth, sib) -> np.ndarray:
     raise ValueError(rule)
 
 
+def accepted_prefix(rng: np.random.Generator, parent, sib, q=(0.55, 0.2, 0.1, 0.05)) -> np.ndarray:
+    """Synthetic verification outcome of one draft tree (or chain): starting at
+    the root, the verifier takes the child of sibling rank r with probability
+    q[r] (nothing with the remaining mass) and continues from it.  Returns a
+    0/1 mask of the nodes on the accepted output prefix (the root included).
+    One uniform draw per visited node; a node's marginal chance to be on the
+    prefix is the product of q over the ranks along its path."""
+    T = len(parent)
+    on = np.zeros(T, np.uint8)
+    if T == 0:
+        return on
+    kids = [[] for _ in range(T)]
+    for t in range(T):
+        if parent[t] >= 0:
+            kids[int(parent[t])].append(t)
+    node = 0
+    on[0] = 1
+    while kids[node]:
+        u = rng.random()
+        nxt, acc = -1, 0.0
+        for c in sorted(kids[node], key=lambda c: sib[c]):
+            r = int(sib[c])
+            acc += q[r] if r < len(q) else 0.0
+            if u < acc:
+                nxt = c
+                break
+        if nxt < 0:
+            break
+        on[nxt] = 1
+        node = nxt
+    return on
+
+
 def correlated_hidden(rng: np.random.Generator, parent, H: int, std: float, rho: float,
                       root=None) -> np.ndarray:
     """fp32 hidden states along the tree: child = rho*parent + sqrt(1-rho^2)*eps.
