@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--trace-warmup", type=int, default=16, help="leading trace blocks not counted")
     ap.add_argument("--rho-step", type=float, default=0.9, help="root correlation of consecutive trace blocks")
     ap.add_argument("--phys-layers", type=int, default=4, help="layers of the physical (copying) offload run")
+    ap.add_argument("--estimate", action="store_true",
+                    help="offline commitment estimator report (p_hat from synthetic traces, tree and chain blocks)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="only run a plain device copy of MB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -106,6 +108,9 @@ def main():
         return
     if args.offload:
         offload_report(args)
+        return
+    if args.estimate:
+        estimate_report(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this layer runs on a single MI355X "
@@ -561,6 +566,73 @@ def offload_report(args):
                   "hit_rate_change_pp": round(100.0 * (am["hit_rate"] - sd["hit_rate"]), 1)},
               "timing": "wall clock of eager steps (route, select, host round trip, loads, forward)",
               "data": "synthetic"}
+    print(json.dumps(report), flush=True)
+
+
+def estimate_report(args):
+    """Offline commitment estimator (Sec. 3.2) on synthetic verification traces.
+
+    Training split: 2000 draft trees (60 nodes, Qwen3-30B-A3B stack shape) and
+    2000 chains of 8, each verified by the synthetic acceptance process (the
+    verifier takes the sibling of rank r with probability (0.55, 0.2, 0.1,
+    0.05)[r]); the library accumulates m_d, c_d and returns p_hat.  Held-out
+    split: 64 blocks of each shape selected on the GPU with p_t = p_hat[d_t]
+    (expanded on the device) and, for comparison, with the fixed synthetic
+    probabilities 0.75^d 0.6^r; |S|, |S'| and routed experts are reported.
+    """
+    import torch
+
+    from paper_2608_02989_amd import _lib as L
+    from paper_2608_02989_amd import ops
+    from paper_2608_02989_amd import workload as W
+
+    t0 = time.time()
+
+    def log(msg):
+        print(f"[estimate {time.time() - t0:6.1f}s] {msg}", file=sys.stderr, flush=True)
+
+    dev = "cuda"
+    cfg = W.CONFIGS["qwen3_30b_a3b_x48"]
+    shapes = {"tree": (9, lambda b: W.make_tree(np.random.default_rng(10_000 + b), cfg.T, cfg.depth_max)),
+              "chain": (8, lambda b: W.chain(8))}
+    n_train, n_eval = 2000, 64
+    report = {"report": "offline commitment estimator on synthetic verification traces", "config": cfg.name,
+              "acceptance_q": [0.55, 0.2, 0.1, 0.05], "train_blocks": n_train, "eval_blocks": n_eval, "shapes": {}}
+    router = ops.pack_router_weights(torch.from_numpy(W.router_weights(cfg, 0)).to(dev))
+    for name, (D, make) in shapes.items():
+        est = ops.CommitEstimator(D)
+        rng = np.random.default_rng(77)
+        trees = [make(b) for b in range(n_train)]
+        outcomes = [W.accepted_prefix(rng, par, sib) for par, dep, sib in trees]
+        nodes = sum(len(t[0]) for t in trees)
+        t1 = time.perf_counter()
+        for (par, dep, sib), on in zip(trees, outcomes):
+            est.add(dep, on)
+        t_count = time.perf_counter() - t1
+        p_hat = est.estimate()
+        log(f"{name}: p_hat {np.round(p_hat, 4).tolist()}")
+        p_hat_dev = torch.from_numpy(p_hat).to(dev)
+        stats = {"estimated": [], "synthetic": []}
+        for b in range(n_eval):
+            par, dep, sib = make(n_train + b)
+            h32 = W.correlated_hidden(W.rng_for(cfg.cfg_id, n_train + b, 0, W.STREAM_HIDDEN), par, cfg.H,
+                                      cfg.hidden_std, args.rho)
+            h = torch.from_numpy(W.bf16_round(h32).view(np.int16)).view(torch.bfloat16).to(dev)
+            logits = ops.route(h, router)
+            par_d, dep_d = torch.from_numpy(par).to(dev), torch.from_numpy(dep).to(dev)
+            synth = torch.from_numpy(W.commit_probs(None, "depth_sibling", dep, sib)).to(dev)
+            for kind, prob in (("estimated", ops.commit_expand(p_hat_dev, dep_d)), ("synthetic", synth)):
+                out = ops.select(logits, par_d, dep_d, prob, None, cfg.k)
+                stats[kind].append(out["stats"][0].cpu().numpy().copy())
+        sh = {"D": D, "p_hat": [round(float(x), 5) for x in p_hat], "m": est.m.tolist(), "c": est.c.tolist(),
+              "train_nodes": int(nodes), "count_ns_per_node": round(t_count / nodes * 1e9, 1)}
+        for kind, rows in stats.items():
+            st = np.asarray(rows, np.float64)
+            sh[kind] = {"S": _dist(st[:, 3]), "S_prime": _dist(st[:, 4]), "natural_union": _dist(st[:, 5]),
+                        "routed": _dist(st[:, 9]), "n_er": _dist(st[:, 2])}
+        report["shapes"][name] = sh
+        log(f"{name}: |S'| estimated {sh['estimated']['S_prime']['mean']} synthetic {sh['synthetic']['S_prime']['mean']}")
+    report["data"] = "synthetic"
     print(json.dumps(report), flush=True)
 
 

@@ -249,6 +249,33 @@ int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_g
 
 /*
  * ---------------------------------------------------------------------------
+ * Offline commitment estimator (Sec. 3.2)
+ * ---------------------------------------------------------------------------
+ * p_hat_d = c_d / m_d over verification traces: m_d counts the proposed nodes
+ * at draft position d (tree depth, or block offset for a chain), c_d those on
+ * the accepted output prefix -- a marginal commitment probability.  The table
+ * is fixed offline; acceptmoe_commit_expand turns it into the per-node
+ * commit_prob that acceptmoe_select takes (p_t = p_hat[d_t]).
+ *
+ * acceptmoe_commit_count -- accumulates one block: for every node t with
+ *   0 <= depth[t] < D, m[d] += 1 and c[d] += (on_path[t] != 0).  Host arrays:
+ *   depth int32 [T], on_path uint8 [T], m and c int64 [D] (caller zeroes them
+ *   before the first block).
+ * acceptmoe_commit_estimate -- p_hat[d] = c[d] / m[d] computed in double and
+ *   rounded once to float, 0 where m[d] == 0.  Host arrays; rejects c > m or
+ *   negative counts.
+ * acceptmoe_commit_expand -- prob[t] = p_hat[depth[t]], 0 for depths outside
+ *   [0, D).  Device arrays p_hat float [D], depth int32 [T], prob float [T];
+ *   asynchronous on `stream`.
+ */
+int32_t acceptmoe_commit_count(const int32_t* depth, const uint8_t* on_path, int32_t T, int32_t D,
+                               int64_t* m, int64_t* c);
+int32_t acceptmoe_commit_estimate(const int64_t* m, const int64_t* c, int32_t D, float* p_hat);
+int32_t acceptmoe_commit_expand(const float* p_hat, int32_t D, const int32_t* depth, int32_t T,
+                                float* prob, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
  * Physical expert offload (Sec. 3.4, offload paragraph; Sec. 4, offload setup)
  * ---------------------------------------------------------------------------
  * Each MoE layer keeps an X-slot expert pool in device memory and the packed

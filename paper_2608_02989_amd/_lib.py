@@ -54,6 +54,9 @@ SIGNATURES = {
     "acceptmoe_pack_gate_up_weights": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp]),
     "acceptmoe_moe_forward": (_i32, [_vp, _i32, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp,
                                      _vp, _vp, _sz, _vp]),
+    "acceptmoe_commit_count": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
+    "acceptmoe_commit_estimate": (_i32, [_vp, _vp, _i32, _vp]),
+    "acceptmoe_commit_expand": (_i32, [_vp, _i32, _vp, _i32, _vp, _vp]),
     "acceptmoe_pool_state_bytes": (_sz, [_i32, _i32]),
     "acceptmoe_pool_init": (_i32, [_vp, _sz, _i32, _i32]),
     "acceptmoe_pool_resident_mask": (_i32, [_vp, _vp]),

@@ -21,7 +21,7 @@ extern "C" {
 
 const char* acceptmoe_last_error(void) { return amoe::abi::g_err; }
 
-int32_t acceptmoe_version(void) { return 300; }
+int32_t acceptmoe_version(void) { return 301; }
 
 // ---------------------------------------------------------------------------
 size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H) {

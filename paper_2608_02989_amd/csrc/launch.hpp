@@ -47,6 +47,8 @@ struct SelectParams {
 size_t select_workspace_bytes(int T, int E, int k);
 void select_carve(void* ws, int T, int E, int k, SelectParams& p);
 hipError_t launch_select(const SelectParams& p, const TreeOffsets& offs, hipStream_t stream);
+hipError_t launch_commit_expand(const float* p_hat, int D, const int32_t* depth, int T, float* prob,
+                                hipStream_t stream);
 
 // ---- expert FFN (forward.hip) ----
 hipError_t launch_pack(const void* src, int is_bf16, int E, int N, int K, void* dst, hipStream_t stream);

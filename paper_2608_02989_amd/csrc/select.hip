@@ -729,6 +729,23 @@ hipError_t launch_select_epl(const SelectParams& p, const TreeOffsets& offs, hip
   return hipGetLastError();
 }
 
+// prob[t] = p_hat[depth[t]] (0 outside the table)
+__global__ void commit_expand_kernel(const float* __restrict__ p_hat, int D, const int32_t* __restrict__ depth, int T,
+                                     float* __restrict__ prob) {
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < T; t += gridDim.x * blockDim.x) {
+    const int d = depth[t];
+    prob[t] = (d >= 0 && d < D) ? p_hat[d] : 0.0f;
+  }
+}
+
+hipError_t launch_commit_expand(const float* p_hat, int D, const int32_t* depth, int T, float* prob,
+                                hipStream_t stream) {
+  const int block = 256;
+  const int grid = min((T + block - 1) / block, 1024);
+  commit_expand_kernel<<<grid, block, 0, stream>>>(p_hat, D, depth, T, prob);
+  return hipGetLastError();
+}
+
 hipError_t launch_select(const SelectParams& p, const TreeOffsets& offs, hipStream_t stream) {
   const int epl = (p.E + kWave - 1) / kWave;
   if (epl <= 1) return launch_select_epl<1>(p, offs, stream);

@@ -386,3 +386,39 @@ class OffloadLayer:
             if nw > 1:
                 copy_rows(target, out, self.wave_tag[:T], w)
         return outs, out, wave_of
+
+
+# ---------------------------------------------------------------------------
+# offline commitment estimator (acceptmoe_commit_*)
+# ---------------------------------------------------------------------------
+class CommitEstimator:
+    """Accumulates m_d / c_d over verification traces and turns them into the
+    p_hat table (Sec. 3.2); host arrays, the library does the counting."""
+
+    def __init__(self, D: int):
+        self.D = D
+        self.m = np.zeros(D, np.int64)
+        self.c = np.zeros(D, np.int64)
+
+    def add(self, depth, on_path):
+        depth = np.ascontiguousarray(depth, np.int32)
+        on_path = np.ascontiguousarray(on_path, np.uint8)
+        check(lib().acceptmoe_commit_count(_host_ptr(depth), _host_ptr(on_path), len(depth), self.D,
+                                           _host_ptr(self.m), _host_ptr(self.c)))
+
+    def estimate(self) -> np.ndarray:
+        p = np.zeros(self.D, np.float32)
+        check(lib().acceptmoe_commit_estimate(_host_ptr(self.m), _host_ptr(self.c), self.D, _host_ptr(p)))
+        return p
+
+
+def commit_expand(p_hat: torch.Tensor, depth: torch.Tensor, out: torch.Tensor | None = None,
+                  stream=None) -> torch.Tensor:
+    """Per-node commitment probabilities p_t = p_hat[d_t] on the device (acceptmoe_commit_expand)."""
+    _need(p_hat, "p_hat", torch.float32, 1)
+    _need(depth, "depth", torch.int32, 1)
+    if out is None:
+        out = torch.empty(depth.shape[0], dtype=torch.float32, device=depth.device)
+    check(lib().acceptmoe_commit_expand(_ptr(p_hat), p_hat.shape[0], _ptr(depth), depth.shape[0], _ptr(out),
+                                        _stream_ptr(stream)))
+    return out
