@@ -328,14 +328,15 @@ def _dist(x):
 
 
 def stack_report(args, cfg):
-    """Eligible-set sizes of a 48-layer stack over many seeded blocks, and the
-    latency of a full verify pass through all layers.
+    """The 48-layer verify pass: layers chained by the residual stream
+    (h_{l+1} = h_l + y_l rounded to bf16), each with its own router and
+    experts (all 48 layers resident, 54 GiB).
 
-    Every (block, layer) pair gets the block's tree (shared by all layers) and
-    its own hidden states and router; route + select run on the GPU and the
-    per-tree statistics are collected on the device.  Then `--stack-blocks`
-    blocks are pushed through all layers (route, select, forward each) with
-    every layer's experts resident.
+    Part 1: eligible-set sizes of every (block, layer) pair over many seeded
+    blocks run through the chained stack.  Part 2: latency of a whole pass per
+    block -- eager launches, one HIP graph for the whole 48-layer pass, and two
+    blocks in flight on two streams (one block's latency-bound selection chain
+    overlapping the other's bandwidth-bound expert FFN).
     """
     import torch
 
@@ -351,74 +352,126 @@ def stack_report(args, cfg):
     dev = "cuda"
     nblocks = args.blocks if args.blocks != 16 else cfg.blocks
     nl = cfg.layers
-    T, E, k = cfg.T, cfg.E, cfg.k
-    routers = [ops.pack_router_weights(torch.from_numpy(W.router_weights(cfg, l)).to(dev)) for l in range(nl)]
-    logits = torch.empty((T, E), dtype=torch.float32, device=dev)
-    ws = ops.select_workspace(T, E, k, dev)
+    T, k = cfg.T, cfg.k
+    layers = []
+    for l in range(nl):
+        wg, wu, wd = W.expert_weights_torch(cfg, l, dev)
+        layers.append(ops.VerifyLayer(torch.from_numpy(W.router_weights(cfg, l)).to(dev), wg, wu, wd, k,
+                                      max_tokens=T))
+        del wg, wu, wd
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    stack = ops.VerifyStack(layers, T)
+    log(f"{nl} layers packed")
+
+    def block(b):
+        blk = W.make_block(cfg, block=b, layer=0, rho=args.rho, tree_layer=0)
+        h = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(dev)
+        return (h,) + tuple(torch.from_numpy(a).to(dev) for a in (blk.parent, blk.depth, blk.prob))
+
     stats_all = torch.empty((nblocks, nl, L.NUM_STATS), dtype=torch.int32, device=dev)
-    outs = {"eligible": torch.empty((1, E), dtype=torch.uint8, device=dev),
-            "idx": torch.empty((T, k), dtype=torch.int32, device=dev),
-            "gate": torch.empty((T, k), dtype=torch.float32, device=dev)}
+    routed_bytes = []
     for b in range(nblocks):
+        h, par, dep, prob = block(b)
+        stack.step(h, par, dep, prob)
         for l in range(nl):
-            blk = W.make_block(cfg, block=b, layer=l, rho=args.rho, tree_layer=0)
-            h = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(dev)
-            par, dep, prob = (torch.from_numpy(a).to(dev) for a in (blk.parent, blk.depth, blk.prob))
-            ops.route(h, routers[l], out=logits)
-            outs["stats"] = stats_all[b, l:l + 1]
-            ops.select(logits, par, dep, prob, None, k, workspace=ws, outputs=outs)
+            stats_all[b, l].copy_(layers[l].sel_out["stats"][0])
         if b % 32 == 31:
-            log(f"{b + 1} blocks selected")
+            log(f"{b + 1} blocks through the chained stack")
     torch.cuda.synchronize()
     st = stats_all.cpu().numpy().reshape(-1, L.NUM_STATS).astype(np.float64)
     assert (st[:, 8] == 0).all(), "malformed synthetic tree"
     sp, un, routed, ner = st[:, 4], st[:, 5], st[:, 9], st[:, 2]
-    report = {"report": "eligible-set size distribution", "config": cfg.name, "blocks": nblocks,
-              "layers": nl, "samples": int(st.shape[0]), "T": T, "H": cfg.H, "E": E, "k": k,
+    report = {"report": "48-layer verify pass (residual-chained layers)", "config": cfg.name, "blocks": nblocks,
+              "layers": nl, "samples": int(st.shape[0]), "T": T, "H": cfg.H, "E": cfg.E, "k": k,
               "rho": args.rho, "eligible_S_prime": _dist(sp), "natural_union": _dist(un),
               "ratio_S_prime_over_U_nat": _dist(sp / un), "routed_experts": _dist(routed),
               "n_er": _dist(ner)}
     log(f"|S'| mean {sp.mean():.2f}, |U_nat| mean {un.mean():.2f}")
 
-    # full 48-layer verify pass for a few blocks, all layers' experts resident
-    layers = []
-    for l in range(nl):
-        wg, wu, wd = W.expert_weights_torch(cfg, l, dev)
-        layers.append(ops.VerifyLayer(routers[l], wg, wu, wd, k, max_tokens=T))
-        del wg, wu, wd
-    torch.cuda.synchronize()
-    torch.cuda.empty_cache()
-    log("48 layers packed")
     nb = args.stack_blocks
-    inputs = []
-    for b in range(nb):
-        per = []
-        for l in range(nl):
-            blk = W.make_block(cfg, block=b, layer=l, rho=args.rho, tree_layer=0)
-            h = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(dev)
-            per.append((h,) + tuple(torch.from_numpy(a).to(dev) for a in (blk.parent, blk.depth, blk.prob)))
-        inputs.append(per)
-    for l in range(nl):
-        layers[l].step(*inputs[0][l])
+    inputs = [block(b) for b in range(nb)]
+    pass_bytes = float(np.mean(routed[:nb * nl].reshape(nb, nl).sum(1))) * cfg.expert_bytes
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    # eager, one stream
+    stack.step(*inputs[0])
     torch.cuda.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
+    e0, e1 = ev(), ev()
+    e0.record()
     for b in range(nb):
-        for l in range(nl):
-            layers[l].step(*inputs[b][l])
-    stop.record()
+        stack.step(*inputs[b])
+    e1.record()
     torch.cuda.synchronize()
-    total_us = start.elapsed_time(stop) * 1e3
-    byts = 0.0
+    eager_us = e0.elapsed_time(e1) * 1e3 / nb
+
+    # one HIP graph per 48-layer pass; the block's inputs are copied into its buffers
+    cap = tuple(torch.empty_like(x) for x in inputs[0])
+    s = torch.cuda.Stream()
+    for dst, src in zip(cap, inputs[0]):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        stack.step(*cap)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        stack.step(*cap)
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record()
     for b in range(nb):
-        for l in range(nl):
-            layers[l].step(*inputs[b][l])
-            idx = layers[l].sel_out["idx"][:T]
-            byts += int(torch.unique(idx[idx >= 0]).numel()) * cfg.expert_bytes
-    report.update({"stack_pass_blocks": nb, "stack_pass_us_per_block": round(total_us / nb, 1),
-                   "stack_pass_us_per_layer": round(total_us / nb / nl, 2),
-                   "stack_pass_weight_GBs": round(byts / (total_us * 1e-6) / 1e9, 1),
-                   "timing": "eager launches, 48 distinct resident layers per block"})
+        for dst, src in zip(cap, inputs[b]):
+            dst.copy_(src)
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    graph_us = e0.elapsed_time(e1) * 1e3 / nb
+
+    # two blocks in flight: two graphs over twin buffers, replayed on two streams
+    twin = stack.twin()
+    cap2 = tuple(torch.empty_like(x) for x in inputs[0])
+    s2 = torch.cuda.Stream()
+    for dst, src in zip(cap2, inputs[1 % nb]):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s2):
+        twin.step(*cap2)
+    torch.cuda.synchronize()
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2, stream=s2):
+        twin.step(*cap2)
+    torch.cuda.synchronize()
+    main = torch.cuda.current_stream()
+    e0, e1 = ev(), ev()
+    e0.record()
+    for b in range(0, nb - 1, 2):
+        s.wait_stream(main)
+        s2.wait_stream(main)
+        with torch.cuda.stream(s):
+            for dst, src in zip(cap, inputs[b]):
+                dst.copy_(src)
+            g.replay()
+        with torch.cuda.stream(s2):
+            for dst, src in zip(cap2, inputs[b + 1]):
+                dst.copy_(src)
+            g2.replay()
+        main.wait_stream(s)
+        main.wait_stream(s2)
+    e1.record()
+    torch.cuda.synchronize()
+    pairs = (nb // 2) * 2
+    two_us = e0.elapsed_time(e1) * 1e3 / max(pairs, 1)
+    report.update({"stack_pass_blocks": nb, "eager_us_per_block": round(eager_us, 1),
+                   "graph_us_per_block": round(graph_us, 1), "graph_us_per_layer": round(graph_us / nl, 2),
+                   "two_stream_us_per_block": round(two_us, 1),
+                   "routed_MB_per_pass": round(pass_bytes / 1e6, 1),
+                   "graph_weight_GBs": round(pass_bytes / (graph_us * 1e-6) / 1e9, 1),
+                   "two_stream_weight_GBs": round(pass_bytes / (two_us * 1e-6) / 1e9, 1),
+                   "timing": "HIP events; 48 distinct resident layers per pass; two-stream figure is "
+                             "throughput with two blocks in flight"})
+    log(f"pass per block: eager {eager_us:.0f} us, graph {graph_us:.0f} us, two streams {two_us:.0f} us")
     print(json.dumps(report), flush=True)
 
 

@@ -248,6 +248,17 @@ int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_g
                               size_t workspace_bytes, void* stream);
 
 /*
+ * acceptmoe_residual_add -- out = hidden + y, rounded to `dtype` (bf16: the
+ * fp32 sum rounded to nearest even; fp32: the plain sum).  Chains stacked
+ * verify layers: the next layer's input is the previous one's input plus its
+ * MoE output (the residual stream of the target stack; attention is not part
+ * of this library).  hidden and out [T, H] of `dtype` (out may equal hidden),
+ * y [T, H] fp32, all device and 16-byte aligned; H % 4 == 0.
+ */
+int32_t acceptmoe_residual_add(const void* hidden, int32_t dtype, const float* y, int32_t T,
+                               int32_t H, void* out, void* stream);
+
+/*
  * ---------------------------------------------------------------------------
  * Offline commitment estimator (Sec. 3.2)
  * ---------------------------------------------------------------------------

@@ -54,6 +54,7 @@ SIGNATURES = {
     "acceptmoe_pack_gate_up_weights": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp]),
     "acceptmoe_moe_forward": (_i32, [_vp, _i32, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp,
                                      _vp, _vp, _sz, _vp]),
+    "acceptmoe_residual_add": (_i32, [_vp, _i32, _vp, _i32, _i32, _vp, _vp]),
     "acceptmoe_commit_count": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "acceptmoe_commit_estimate": (_i32, [_vp, _vp, _i32, _vp]),
     "acceptmoe_commit_expand": (_i32, [_vp, _i32, _vp, _i32, _vp, _vp]),

@@ -21,7 +21,7 @@ extern "C" {
 
 const char* acceptmoe_last_error(void) { return amoe::abi::g_err; }
 
-int32_t acceptmoe_version(void) { return 301; }
+int32_t acceptmoe_version(void) { return 302; }
 
 // ---------------------------------------------------------------------------
 size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H) {
@@ -252,6 +252,21 @@ int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_g
   amoe::forward_carve(workspace, p);
   hipError_t e = amoe::launch_forward(p, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "forward launch");
+}
+
+int32_t acceptmoe_residual_add(const void* hidden, int32_t dtype, const float* y, int32_t T, int32_t H, void* out,
+                               void* stream) {
+  clear_err();
+  if (dtype != ACCEPTMOE_F32 && dtype != ACCEPTMOE_BF16)
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "residual_add: unknown dtype %d", dtype);
+  if (T < 0 || H < 1) return fail(ACCEPTMOE_ERR_INVALID_ARG, "residual_add: bad sizes (T=%d H=%d)", T, H);
+  if (H % 4 != 0) return fail(ACCEPTMOE_ERR_UNSUPPORTED, "residual_add: H must be a multiple of 4 (got %d)", H);
+  if (T == 0) return ACCEPTMOE_OK;
+  if (!hidden || !y || !out) return fail(ACCEPTMOE_ERR_INVALID_ARG, "residual_add: null pointer");
+  if (!aligned(hidden, 16) || !aligned(y, 16) || !aligned(out, 16))
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "residual_add: pointers must be 16-byte aligned");
+  hipError_t e = amoe::launch_residual_add(hidden, dtype == ACCEPTMOE_BF16, y, T, H, out, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "residual_add launch");
 }
 
 }  // extern "C"

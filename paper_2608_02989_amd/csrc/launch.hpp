@@ -53,6 +53,8 @@ hipError_t launch_commit_expand(const float* p_hat, int D, const int32_t* depth,
 // ---- expert FFN (forward.hip) ----
 hipError_t launch_pack(const void* src, int is_bf16, int E, int N, int K, void* dst, hipStream_t stream);
 size_t packed_gate_up_bytes(int is_bf16, int E, int I, int H);
+hipError_t launch_residual_add(const void* hidden, int is_bf16, const float* y, int T, int H, void* out,
+                               hipStream_t stream);
 hipError_t launch_copy_rows(const float* src, float* dst, const int32_t* row_tag, int tag, int T, int H,
                             hipStream_t stream);
 hipError_t launch_pack_gate_up(const void* gate, const void* up, int is_bf16, int E, int I, int H, void* dst,

@@ -6,6 +6,7 @@ other than OK and RuntimeError when the library is missing.
 """
 from __future__ import annotations
 
+import copy
 import ctypes
 
 import numpy as np
@@ -214,8 +215,11 @@ class VerifyLayer:
         self.dtype = w_gate.dtype
         self.wgu = pack_gate_up_weights(w_gate, w_up)
         self.wd = pack_expert_weights(w_down)
-        dev = w_gate.device
-        T = max_tokens
+        self._alloc(max_tokens, max_trees, w_gate.device)
+
+    def _alloc(self, max_tokens: int, max_trees: int, dev):
+        T, k = max_tokens, self.k
+        self.max_tokens, self.max_trees = max_tokens, max_trees
         self.logits = torch.empty((T, self.E), dtype=torch.float32, device=dev)
         self.sel_ws = select_workspace(T, self.E, k, dev)
         self.fwd_ws = forward_workspace(T, self.H, self.I, self.E, k, self.dtype, dev)
@@ -226,6 +230,13 @@ class VerifyLayer:
             "stats": torch.empty((max_trees, L.NUM_STATS), dtype=torch.int32, device=dev),
         }
         self.out = torch.empty((T, self.H), dtype=torch.float32, device=dev)
+
+    def twin(self) -> "VerifyLayer":
+        """The same layer (shared packed weights) with its own workspaces and
+        outputs, for a second block in flight on another stream."""
+        other = copy.copy(self)
+        other._alloc(self.max_tokens, self.max_trees, self.logits.device)
+        return other
 
     def step(self, hidden, parent, depth, prob, tree_offsets=None, resident=None, stream=None):
         T = hidden.shape[0]
@@ -240,6 +251,52 @@ class VerifyLayer:
         moe_forward(hidden, self.wgu, self.wd, outs["idx"], outs["gate"], out=out,
                     workspace=self.fwd_ws, stream=stream)
         return logits, outs, out
+
+
+def residual_add(hidden: torch.Tensor, y: torch.Tensor, out: torch.Tensor | None = None,
+                 stream=None) -> torch.Tensor:
+    """out = hidden + y rounded to hidden's dtype (acceptmoe_residual_add)."""
+    _need(hidden, "hidden", dim=2)
+    _need(y, "y", torch.float32, 2)
+    if y.shape != hidden.shape:
+        raise ValueError("residual_add: hidden and y must have the same shape")
+    if out is None:
+        out = torch.empty_like(hidden)
+    T, H = hidden.shape
+    check(lib().acceptmoe_residual_add(_ptr(hidden), _dtype_code(hidden), _ptr(y), T, H, _ptr(out),
+                                       _stream_ptr(stream)))
+    return out
+
+
+class VerifyStack:
+    """Verify layers chained by the residual stream, h_{l+1} = h_l + y_l rounded
+    to the layer dtype (attention between the MoE layers is not modelled).
+
+    step() runs route -> select -> forward -> residual add for every layer on
+    one stream and allocates nothing, so a whole pass can be captured in one
+    HIP graph.  The input of every layer stays in `h[l]` and each layer's
+    logits, routing and output in its own buffers (for teacher-forced checks).
+    """
+
+    def __init__(self, layers: list, max_tokens: int):
+        self.layers = layers
+        dev = layers[0].logits.device
+        self.h = [torch.empty((max_tokens, layers[0].H), dtype=layers[0].dtype, device=dev)
+                  for _ in range(len(layers) + 1)]
+
+    def twin(self) -> "VerifyStack":
+        """Same weights, own buffers (a second block in flight)."""
+        return VerifyStack([ly.twin() for ly in self.layers], self.h[0].shape[0])
+
+    def step(self, h0, parent, depth, prob, tree_offsets=None, stream=None) -> torch.Tensor:
+        T = h0.shape[0]
+        if h0.data_ptr() != self.h[0].data_ptr():
+            with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream()):
+                self.h[0][:T].copy_(h0)
+        for l, layer in enumerate(self.layers):
+            _, _, y = layer.step(self.h[l][:T], parent, depth, prob, tree_offsets, stream=stream)
+            residual_add(self.h[l][:T], y, out=self.h[l + 1][:T], stream=stream)
+        return self.h[len(self.layers)][:T]
 
 
 # ---------------------------------------------------------------------------

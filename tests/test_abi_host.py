@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_error_string():
-    assert L.lib().acceptmoe_version() == 301
+    assert L.lib().acceptmoe_version() == 302
     assert isinstance(L.lib().acceptmoe_last_error(), bytes)
 
 
