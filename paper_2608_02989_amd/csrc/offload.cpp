@@ -193,7 +193,9 @@ int32_t acceptmoe_pool_serve_wave(void* state, const int32_t* topk_idx, const in
         if (held >= 0 && needed[held]) continue;
         if (best < 0 || v.stamp[j] < v.stamp[best]) best = j;
       }
-      s = best;  // exists: the wave's union fits in X slots
+      if (best < 0)  // cannot happen while the wave's union fits in X slots (checked above)
+        return fail(ACCEPTMOE_ERR_INVALID_ARG, "pool_serve_wave: no slot to evict for expert %d", e);
+      s = best;
       if (v.expert_in[s] >= 0) v.slot_of[v.expert_in[s]] = -1;
       v.expert_in[s] = e;
       v.slot_of[e] = s;
