@@ -21,7 +21,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libacceptmoe.so"
 ARCH = os.environ.get("ACCEPTMOE_ARCH", "gfx950")
 
-SOURCES = ["route.hip", "select.hip", "forward.hip", "api.cpp", "offload.cpp", "estimate.cpp"]
+SOURCES = ["route.hip", "select.hip", "forward.hip", "stream_kernels.hip", "api.cpp", "offload.cpp", "estimate.cpp"]
 
 COMMON_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
