@@ -83,20 +83,25 @@ extern "C" {
 
 /*
  * acceptmoe_packed_router_bytes -- bytes of a packed router matrix:
- *   ceil(E / 16) * 16 * H * 4 (0 for unsupported E or H).
+ *   ceil(E / 16) * 16 * ceil(H / 32) * 32 * 6 (0 for unsupported E or H).
  * acceptmoe_pack_router_weights -- converts the fp32 router matrix W_r
  * [E, H] (nn.Linear orientation, row-major) into the layout acceptmoe_route
- * reads: rows padded with zeros to a multiple of 16, then for every 16-row
- * tile and every 16-column chunk the 16 x 16 block is stored as 64 lanes x
- * 16 B, lane L holding row (L % 16), columns 4*(L / 16) .. +3 of the chunk
- * (the fp32 case of the expert-weight packing).  A one-time, load-time step.
+ * reads.  Each weight w becomes three bf16 values (round to nearest even)
+ * hi = bf16(w), mid = bf16(w - hi), lo = bf16(w - hi - mid), whose sum is w
+ * exactly for |w| above about 1e-33.  Rows are padded with zeros to a
+ * multiple of 16 and columns to a multiple of 32; then for every 16-row tile
+ * et, every 32-column chunk c and every plane p (0 hi, 1 mid, 2 lo) a
+ * fragment of 64 lanes x 16 B follows, lane L holding plane p of row
+ * 16*et + (L % 16), columns 32*c + 8*(L / 16) .. +7 (eight bf16).  Fragment
+ * (et, c, p) starts at byte ((et * ceil(H/32) + c) * 3 + p) * 1024.  A
+ * one-time, load-time step.
  *
  *   src  [E, H] fp32 device;  dst device, acceptmoe_packed_router_bytes(E, H)
  *   bytes, must not overlap src.  1 <= E <= ACCEPTMOE_MAX_EXPERTS,
  *   H >= 16 and H % 16 == 0; both 16-byte aligned.
  */
 size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H);
-int32_t acceptmoe_pack_router_weights(const float* src, int32_t E, int32_t H, float* dst, void* stream);
+int32_t acceptmoe_pack_router_weights(const float* src, int32_t E, int32_t H, void* dst, void* stream);
 
 /*
  * acceptmoe_route -- router logits z_t = W_r h_t for every node of the block
@@ -104,13 +109,15 @@ int32_t acceptmoe_pack_router_weights(const float* src, int32_t E, int32_t H, fl
  *
  *   hidden         [T, H] device, element type `hidden_dtype` (F32 or BF16),
  *                  16-byte aligned
- *   router_packed  W_r [E, H] fp32 in the layout of acceptmoe_pack_router_weights
+ *   router_packed  W_r [E, H] in the layout of acceptmoe_pack_router_weights
  *   logits         [T, E] device fp32, written
  *   T >= 0 (T == 0 is a no-op), 1 <= E <= ACCEPTMOE_MAX_EXPERTS,
  *   H >= 16 and H % 16 == 0.
- * Accumulation is fp32; the result is deterministic (fixed reduction order).
+ * Products are exact (bf16 hidden times each bf16 plane, or fp32 hidden
+ * times the rebuilt fp32 weight) and accumulation is fp32, so the logits
+ * carry fp32 accuracy; the result is deterministic (fixed reduction order).
  */
-int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const float* router_packed,
+int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const void* router_packed,
                         int32_t T, int32_t H, int32_t E, float* logits, void* stream);
 
 /*

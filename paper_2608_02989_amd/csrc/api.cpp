@@ -21,7 +21,7 @@ extern "C" {
 
 const char* acceptmoe_last_error(void) { return amoe::abi::g_err; }
 
-int32_t acceptmoe_version(void) { return 302; }
+int32_t acceptmoe_version(void) { return 303; }
 
 // ---------------------------------------------------------------------------
 size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H) {
@@ -29,7 +29,7 @@ size_t acceptmoe_packed_router_bytes(int32_t E, int32_t H) {
   return amoe::packed_router_bytes(E, H);
 }
 
-int32_t acceptmoe_pack_router_weights(const float* src, int32_t E, int32_t H, float* dst, void* stream) {
+int32_t acceptmoe_pack_router_weights(const float* src, int32_t E, int32_t H, void* dst, void* stream) {
   clear_err();
   if (E < 1 || E > ACCEPTMOE_MAX_EXPERTS)
     return fail(ACCEPTMOE_ERR_UNSUPPORTED, "pack_router: E must be in [1, %d] (got %d)", ACCEPTMOE_MAX_EXPERTS, E);
@@ -46,7 +46,7 @@ int32_t acceptmoe_pack_router_weights(const float* src, int32_t E, int32_t H, fl
   return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "pack_router launch");
 }
 
-int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const float* router_packed, int32_t T,
+int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const void* router_packed, int32_t T,
                         int32_t H, int32_t E, float* logits, void* stream) {
   clear_err();
   if (T < 0) return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: T must be >= 0 (got %d)", T);

@@ -17,8 +17,8 @@ constexpr int kNumStats = 10;
 
 // ---- router (route.hip) ----
 size_t packed_router_bytes(int E, int H);
-hipError_t launch_pack_router(const float* src, int E, int H, float* dst, hipStream_t stream);
-hipError_t launch_route(const void* hidden, int hidden_is_bf16, const float* router_packed, int T, int H,
+hipError_t launch_pack_router(const float* src, int E, int H, void* dst, hipStream_t stream);
+hipError_t launch_route(const void* hidden, int hidden_is_bf16, const void* router_packed, int T, int H,
                         int E, float* logits, hipStream_t stream);
 
 // ---- selection (select.hip) ----

@@ -48,7 +48,7 @@ def _need(t: torch.Tensor, name: str, dtype=None, dim=None):
 
 # ---------------------------------------------------------------------------
 class PackedRouter:
-    """Router matrix W_r [E, H] fp32 in the layout acceptmoe_route reads."""
+    """Router matrix W_r [E, H] (fp32 as three bf16 planes) in the layout acceptmoe_route reads."""
 
     def __init__(self, data: torch.Tensor, E: int, H: int):
         self.data, self.E, self.H = data, E, H
@@ -61,7 +61,7 @@ def pack_router_weights(router_w: torch.Tensor, stream=None) -> PackedRouter:
     n = int(lib().acceptmoe_packed_router_bytes(E, H))
     if n == 0:
         raise ValueError(f"unsupported router shape {tuple(router_w.shape)}")
-    data = torch.empty(n // 4, dtype=torch.float32, device=router_w.device)
+    data = torch.empty(n // 2, dtype=torch.int16, device=router_w.device)
     check(lib().acceptmoe_pack_router_weights(_ptr(router_w), E, H, _ptr(data), _stream_ptr(stream)))
     return PackedRouter(data, E, H)
 

@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_error_string():
-    assert L.lib().acceptmoe_version() == 302
+    assert L.lib().acceptmoe_version() == 303
     assert isinstance(L.lib().acceptmoe_last_error(), bytes)
 
 
@@ -60,8 +60,10 @@ def status_and_msg(rc):
 
 def test_pack_router_sizes_and_rejects():
     lib = L.lib()
-    assert lib.acceptmoe_packed_router_bytes(128, 2048) == 128 * 2048 * 4
-    assert lib.acceptmoe_packed_router_bytes(37, 256) == 48 * 256 * 4     # rows padded to 16
+    # three bf16 planes per weight, rows padded to 16 and columns to 32
+    assert lib.acceptmoe_packed_router_bytes(128, 2048) == 128 * 2048 * 6
+    assert lib.acceptmoe_packed_router_bytes(37, 256) == 48 * 256 * 6
+    assert lib.acceptmoe_packed_router_bytes(16, 48) == 16 * 64 * 6
     assert lib.acceptmoe_packed_router_bytes(0, 256) == 0
     assert lib.acceptmoe_packed_router_bytes(16, 250) == 0
     f = lib.acceptmoe_pack_router_weights

@@ -51,15 +51,22 @@ def u8(a):
 # ---------------------------------------------------------------------------
 # route
 # ---------------------------------------------------------------------------
-ROUTE_CASES = [("fp32_small", None, None), ("qwen3_30b_a3b", None, None), ("wide_offload", None, None),
-               ("batched_8x64", None, None), ("qwen3_30b_a3b", 37, 100), ("batched_8x64", None, 100)]
+ROUTE_CASES = [("fp32_small", None, None, None), ("qwen3_30b_a3b", None, None, None),
+               ("wide_offload", None, None, None), ("batched_8x64", None, None, None),
+               ("qwen3_30b_a3b", 37, 100, None), ("batched_8x64", None, 100, None),
+               # H % 32 == 16: the last packed chunk is half padding; with these H the
+               # hidden state is staged in two blocks, the second holding that one chunk
+               ("fp32_small", None, None, 1040), ("qwen3_30b_a3b", 21, 40, 2064),
+               ("fp32_small", None, 24, 48)]
 
 
-@pytest.mark.parametrize("name,T,E", ROUTE_CASES)
-def test_route_parity(gpu, name, T, E):
+@pytest.mark.parametrize("name,T,E,H", ROUTE_CASES)
+def test_route_parity(gpu, name, T, E, H):
     cfg = W.CONFIGS[name]
     if E is not None:
         cfg = W.LayerConfig(**{**cfg.__dict__, "E": E})
+    if H is not None:
+        cfg = W.LayerConfig(**{**cfg.__dict__, "H": H})
     blk = W.make_block(cfg, block=3, T=T if T else None, B=1 if T else None)
     hdev, h64 = hidden_for(cfg, blk.hidden)
     rw = W.router_weights(cfg)
@@ -122,7 +129,8 @@ def test_select_parity_configs(gpu, name, rho, seed):
 
 
 @pytest.mark.parametrize("E,k,T", [(48, 3, 23), (200, 6, 40), (512, 32, 33), (16, 16, 9), (64, 1, 17),
-                                   (100, 8, 130), (128, 8, 1024)])
+                                   (100, 8, 130), (128, 8, 1024), (128, 8, 64), (128, 8, 65),
+                                   (256, 8, 64), (257, 8, 20)])
 def test_select_parity_shapes(gpu, E, k, T):
     rng = np.random.default_rng(E * 1000 + k)
     par, dep, sib = W.make_tree(rng, T, 10)
@@ -351,22 +359,45 @@ def test_pack_gate_up_layout_documented(gpu):
             assert np.array_equal(frags[fi, lane], want), (fi, lane)
 
 
-def test_pack_router_layout_documented(gpu):
-    # values encode (e, h); rows past E are zero
+def bf16_rne_np(x):
+    """fp32 -> nearest-even bf16, returned as fp32 (written from the formats' definitions)."""
+    b = np.asarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    r = ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint32)
+    return (r << 16).view(np.float32)
+
+
+@pytest.mark.parametrize("kind", ["index", "normal"])
+def test_pack_router_layout_documented(gpu, kind):
+    # E = 20 pads rows to 32; H = 48 pads columns to 64 (the second chunk is half padding)
     E, H = 20, 48
-    e_, h_ = np.meshgrid(np.arange(E), np.arange(H), indexing="ij")
-    src = (e_ * 1000 + h_ + 1).astype(np.float32)
+    if kind == "index":     # values encode (e, h) and need more than one bf16 plane
+        e_, h_ = np.meshgrid(np.arange(E), np.arange(H), indexing="ij")
+        src = (e_ * 1000 + h_ + 1 + 1.0 / 3.0).astype(np.float32)
+    else:
+        src = np.random.default_rng(5).normal(0, 0.02, (E, H)).astype(np.float32)
     rp = ops.pack_router_weights(f32(src))
-    packed = rp.data.cpu().numpy().reshape(-1, 64, 4)     # [fragment][lane][4 floats]
-    nchunk = H // 16
-    assert packed.shape[0] == ((E + 15) // 16) * nchunk
-    for f in range(packed.shape[0]):
+    raw = rp.data.cpu().numpy().view(np.uint16).astype(np.uint32)
+    planes = (raw << 16).view(np.float32).reshape(-1, 3, 64, 8)   # [et*nchunk + c][plane][lane][8]
+    nchunk = (H + 31) // 32
+    assert planes.shape[0] == ((E + 15) // 16) * nchunk
+    seen = np.zeros((E, H), bool)
+    for f in range(planes.shape[0]):
         et, c = divmod(f, nchunk)
         for lane in range(64):
             row = et * 16 + lane % 16
-            cols = c * 16 + 4 * (lane // 16) + np.arange(4)
-            want = src[row, cols] if row < E else np.zeros(4, np.float32)
-            assert np.array_equal(packed[f, lane], want), (f, lane)
+            cols = c * 32 + 8 * (lane // 16) + np.arange(8)
+            hi, mid, lo = planes[f, 0, lane], planes[f, 1, lane], planes[f, 2, lane]
+            if row >= E or cols[0] >= H:
+                assert not hi.any() and not mid.any() and not lo.any(), (f, lane)
+                continue
+            w = src[row, cols]
+            assert np.array_equal(hi, bf16_rne_np(w)), (f, lane)
+            assert np.array_equal(mid, bf16_rne_np(w - hi)), (f, lane)
+            assert np.array_equal(lo, bf16_rne_np((w - hi) - mid)), (f, lane)
+            # the three planes rebuild the fp32 weight exactly
+            assert np.array_equal((hi.astype(np.float64) + mid + lo).astype(np.float32), w), (f, lane)
+            seen[row, cols] = True
+    assert seen.all()
 
 
 def test_pack_layout_documented(gpu):
