@@ -12,9 +12,11 @@
 //   restricted top-k  per node: top-k over S' and renormalised gates   (Eq. 2)
 //
 // Three launches: natural_kernel and restricted_kernel put one wave on each
-// node and spread the nodes over many CUs (the per-node work is bound by
-// instruction issue, so it needs the SIMDs of many CUs); tree_kernel runs one
-// 1024-thread workgroup per tree between them.
+// node and spread the nodes over many CUs; tree_kernel runs one 1024-thread
+// workgroup per tree between them.  The per-node top-k is bound by
+// instruction issue (a 32-step ballot search, fp64 exponentials): a block's
+// nodes on one CU queue behind each other on its four SIMDs, which costs more
+// than the two launches saved by running everything in one workgroup.
 //
 // Top-k is a wave-wide radix select on order-preserving 32-bit keys: the k-th
 // largest key is found bit by bit with ballots, keys above it are taken,
@@ -60,38 +62,96 @@ struct SelShared {
   alignas(16) double pval[kMaxExperts];   // ... and their utilities
 };
 
-// per-wave compaction scratch for top-k slot ordering
-template <int W>
-struct NodeScratchT {
-  alignas(16) uint32_t sk[W][kMaxTopK];
-  alignas(16) int se[W][kMaxTopK];
-  alignas(16) float sz[W][kMaxTopK];
-  alignas(16) double sx[W][kMaxTopK];
+// compaction scratch of one node's top-k (slot ordering)
+struct NodeSlot {
+  alignas(16) uint32_t sk[kMaxTopK];
+  alignas(16) int se[kMaxTopK];
+  alignas(16) float sz[kMaxTopK];
+  alignas(16) double sx[kMaxTopK];
 };
-typedef NodeScratchT<kNodeWaves> NodeScratch;
+struct NodeScratch {
+  NodeSlot s[kNodeWaves];
+};
 
-// k-th largest key among the wave's EPL*64 keys (0 if fewer than k are non-zero).
-template <int EPL>
-__device__ __forceinline__ uint32_t kth_largest(const uint32_t (&key)[EPL], int k) {
-  uint32_t cand = 0u;
-  for (int bit = 31; bit >= 0; --bit) {
-    const uint32_t trial = cand | (1u << bit);
-    int cnt = 0;
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) cnt += popc64(__ballot(key[i] >= trial));
-    if (cnt >= k) cand = trial;
-  }
-  return cand;
+// Wave minimum of 32- or 64-bit keys, broadcast (the DPP steps of dpp::reduce).
+__device__ __forceinline__ uint32_t wave_min_key(uint32_t v) {
+  return dpp::reduce(v, 0xffffffffu, [](uint32_t x, uint32_t y) { return min(x, y); });
+}
+template <int Ctrl, int RowMask = 0xf>
+__device__ __forceinline__ uint64_t mov64(uint64_t old, uint64_t v) {
+  const uint32_t lo = dpp::mov<Ctrl, RowMask>(static_cast<uint32_t>(old), static_cast<uint32_t>(v));
+  const uint32_t hi = dpp::mov<Ctrl, RowMask>(static_cast<uint32_t>(old >> 32), static_cast<uint32_t>(v >> 32));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t wave_min_key(uint64_t v) {
+  const uint64_t id = ~0ull;
+  v = min(v, mov64<dpp::kXor1>(id, v));
+  v = min(v, mov64<dpp::kXor2>(id, v));
+  v = min(v, mov64<dpp::kHalfMirror>(id, v));
+  v = min(v, mov64<dpp::kMirror>(id, v));
+  v = min(v, mov64<dpp::kBcast15, 0xA>(id, v));
+  v = min(v, mov64<dpp::kBcast31, 0xC>(id, v));
+  return (static_cast<uint64_t>(dpp::lane63(static_cast<uint32_t>(v >> 32))) << 32) |
+         dpp::lane63(static_cast<uint32_t>(v));
 }
 
-// Selects the top-k keys of the wave (ties -> lower expert index) and
-// compacts the winners into the wave's scratch in expert-index order: key and
-// expert index, plus put(pos, i) for the caller's own payload of element i.
-// Returns the number selected (min(k, #non-zero keys)).
+// k-th largest key among the wave's EPL*64 keys (32- or 64-bit), for NN
+// nodes at once (0 if fewer than k keys are non-zero).  The key is built from
+// the top bit down: cand grows while at least k keys stay >= cand.  Once
+// exactly k keys are >= cand that count stays k, those keys are the top k and
+// the answer is their smallest, so the search stops at the next check (for
+// logits usually after a third of the bits) and takes that minimum; the
+// result equals the full search.  Bits go in unrolled groups of four with one
+// check per group (a wave issues one instruction at a time: a check per bit
+// would double the cost of a step).  The NN searches are independent; one
+// loop lets their ballot chains interleave.
+template <int EPL, int NN, class Key>
+__device__ __forceinline__ void kth_largest(const Key (&key)[NN][EPL], int k, Key (&cand)[NN]) {
+  constexpr int kBits = 8 * sizeof(Key);
+  int have[NN];  // number of keys >= cand[j]
+#pragma unroll
+  for (int j = 0; j < NN; ++j) {
+    cand[j] = 0;
+    have[j] = EPL * kWave;
+  }
+  for (int b0 = kBits - 1; b0 >= 0; b0 -= 4) {
+    bool open = false;
+#pragma unroll
+    for (int j = 0; j < NN; ++j) open = open || have[j] != k;
+    if (!open) break;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+#pragma unroll
+      for (int j = 0; j < NN; ++j) {
+        const Key trial = cand[j] | (static_cast<Key>(1) << (b0 - d));
+        int cnt = 0;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) cnt += popc64(__ballot(key[j][i] >= trial));
+        if (cnt >= k) {
+          cand[j] = trial;
+          have[j] = cnt;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NN; ++j) {
+    if (have[j] != k) continue;  // the search ran to the last bit: cand is exact
+    Key m = ~static_cast<Key>(0);
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) m = key[j][i] >= cand[j] ? min(m, key[j][i]) : m;
+    cand[j] = wave_min_key(m);
+  }
+}
+
+// Takes the top-k keys of the wave given their threshold thr = k-th largest
+// key (ties -> lower expert index) and compacts the winners into the node's
+// scratch in expert-index order: key and expert index, plus put(pos, i) for
+// the caller's own payload of element i.  Returns the number selected
+// (min(k, #non-zero keys)).
 template <int EPL, class Put>
-__device__ __forceinline__ int wave_topk_compact(const uint32_t (&key)[EPL], int k, int lane, uint32_t* sk,
-                                                 int* se, Put&& put) {
-  const uint32_t thr = kth_largest<EPL>(key, k);
+__device__ __forceinline__ int topk_compact(uint32_t thr, const uint32_t (&key)[EPL], int k, int lane, uint32_t* sk,
+                                            int* se, Put&& put) {
   int greater = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) greater += popc64(__ballot(key[i] > thr));
@@ -199,44 +259,52 @@ __device__ __forceinline__ void load_row(const float* __restrict__ zrow, int E, 
 }
 
 // ---------------------------------------------------------------------------
-// natural top-k and router probabilities of node t (one wave)
+// natural top-k and router probabilities of NN nodes t[j] (one wave).  The
+// caller loads the logit rows into zv.  emit(j, slot, e, r) stores node j's
+// entry of rank `slot`.
 // ---------------------------------------------------------------------------
-template <int EPL>
-__device__ __forceinline__ void natural_node(const SelectParams& p, int t, int lane, uint32_t* sk, int* se,
-                                             double* sx) {
+template <int EPL, int NN, class Emit>
+__device__ __forceinline__ void natural_nodes(const SelectParams& p, const int (&t)[NN], const float (&zv)[NN][EPL],
+                                              int lane, NodeSlot* const (&sl)[NN], Emit&& emit) {
   const int E = p.E, k = p.k;
-  float zv[EPL];
-  uint32_t key[EPL];
-  load_row<EPL>(p.logits + static_cast<size_t>(t) * E, E, lane, zv);
+  uint32_t key[NN][EPL];
+  double ex[NN][EPL];
+  double den[NN];
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) key[i] = (lane + kWave * i) < E ? logit_key(zv[i]) : 0u;
-  // softmax over all E in fp64 (max subtracted)
-  float zmax = zv[0];
+  for (int j = 0; j < NN; ++j) {
 #pragma unroll
-  for (int i = 1; i < EPL; ++i) zmax = fmaxf(zmax, zv[i]);
-  zmax = wave_max_f32(zmax);
-  double ex[EPL];
-  double den = 0.0;
+    for (int i = 0; i < EPL; ++i) key[j][i] = (lane + kWave * i) < E ? logit_key(zv[j][i]) : 0u;
+    // softmax over all E in fp64 (max subtracted)
+    float zmax = zv[j][0];
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    ex[i] = (lane + kWave * i) < E ? exp(static_cast<double>(zv[i]) - static_cast<double>(zmax)) : 0.0;
-    den += ex[i];
-  }
-  den = wave_sum_f64(den);
-  if (p.mode == MODE_MOESPEC) {
+    for (int i = 1; i < EPL; ++i) zmax = fmaxf(zmax, zv[j][i]);
+    zmax = wave_max_f32(zmax);
+    den[j] = 0.0;
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
-      const int e = lane + kWave * i;
-      if (e < E) p.ws_rfull[static_cast<size_t>(t) * E + e] = ex[i] / den;
+      ex[j][i] = (lane + kWave * i) < E ? exp(static_cast<double>(zv[j][i]) - static_cast<double>(zmax)) : 0.0;
+      den[j] += ex[j][i];
     }
+    den[j] = wave_sum_f64(den[j]);
   }
-  const int n = wave_topk_compact<EPL>(key, k, lane, sk, se, [&](int pos, int i) { sx[pos] = ex[i]; });
-  if (lane < n) {
-    const int slot = slot_of(lane, n, sk, se);
-    p.ws_kidx[static_cast<size_t>(t) * k + slot] = se[lane];
-    p.ws_r[static_cast<size_t>(t) * k + slot] = sx[lane] / den;
+  if (p.mode == MODE_MOESPEC) {
+#pragma unroll
+    for (int j = 0; j < NN; ++j)
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) {
+        const int e = lane + kWave * i;
+        if (e < E) p.ws_rfull[static_cast<size_t>(t[j]) * E + e] = ex[j][i] / den[j];
+      }
   }
-  wave_lds_sync();  // the scratch is reused by the wave's next node
+  uint32_t thr[NN];
+  kth_largest<EPL, NN>(key, k, thr);
+#pragma unroll
+  for (int j = 0; j < NN; ++j) {
+    NodeSlot& s = *sl[j];
+    const int n = topk_compact<EPL>(thr[j], key[j], k, lane, s.sk, s.se, [&](int pos, int i) { s.sx[pos] = ex[j][i]; });
+    if (lane < n) emit(j, slot_of(lane, n, s.sk, s.se), s.se[lane], s.sx[lane] / den[j]);
+  }
+  wave_lds_sync();  // the scratch is reused by the wave's next nodes
 }
 
 template <int EPL>
@@ -245,45 +313,83 @@ __global__ __launch_bounds__(kNodeWaves * kWave) void natural_kernel(SelectParam
   const int wave = wave_id(), lane = lane_id();
   const int t = blockIdx.x * kNodeWaves + wave;
   if (t >= p.T) return;
-  natural_node<EPL>(p, t, lane, ns.sk[wave], ns.se[wave], ns.sx[wave]);
+  const int tt[1] = {t};
+  float zv[1][EPL];
+  load_row<EPL>(p.logits + static_cast<size_t>(t) * p.E, p.E, lane, zv[0]);
+  NodeSlot* const sl[1] = {&ns.s[wave]};
+  natural_nodes<EPL, 1>(p, tt, zv, lane, sl, [&](int, int slot, int e, double r) {
+    p.ws_kidx[static_cast<size_t>(t) * p.k + slot] = e;
+    p.ws_r[static_cast<size_t>(t) * p.k + slot] = r;
+  });
 }
 
 // ---------------------------------------------------------------------------
-// restricted top-k over the eligible set and renormalised gates of node t
-// (one wave).  elig[e] != 0 marks e in S'.  Experts that receive the node are
-// marked in `routed` (an LDS bitmask of the workgroup).
+// restricted top-k over the eligible set and renormalised gates of NN nodes
+// of one tree (one wave).  elig[e] != 0 marks e in S'.  Nodes with live[j]
+// false are computed and not written.  Experts that receive a node are marked
+// in `routed` (an LDS bitmask).
 // ---------------------------------------------------------------------------
-template <int EPL>
-__device__ __forceinline__ void restricted_node(const SelectParams& p, int t, const uint8_t* elig, int lane,
-                                                uint32_t* sk, int* se, float* sz, uint32_t* routed) {
+template <int EPL, int NN>
+__device__ __forceinline__ void restricted_nodes(const SelectParams& p, const int (&t)[NN], const bool (&live)[NN],
+                                                 const float (&zv)[NN][EPL], const uint8_t* elig, int lane,
+                                                 NodeSlot* const (&sl)[NN], uint32_t* routed) {
   const int E = p.E, k = p.k;
-  float zv[EPL];
-  uint32_t key[EPL];
-  load_row<EPL>(p.logits + static_cast<size_t>(t) * E, E, lane, zv);
+  uint32_t key[NN][EPL];
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    const int e = lane + kWave * i;
-    key[i] = (e < E && elig[e]) ? logit_key(zv[i]) : 0u;
+  for (int j = 0; j < NN; ++j)
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = lane + kWave * i;
+      key[j][i] = (e < E && elig[e]) ? logit_key(zv[j][i]) : 0u;
+    }
+  uint32_t thr[NN];
+  kth_largest<EPL, NN>(key, k, thr);
+#pragma unroll
+  for (int j = 0; j < NN; ++j) {
+    NodeSlot& s = *sl[j];
+    const int n = topk_compact<EPL>(thr[j], key[j], k, lane, s.sk, s.se, [&](int pos, int i) { s.sz[pos] = zv[j][i]; });
+    // gates: softmax over the selected logits, fp64
+    double zm = lane < n ? static_cast<double>(s.sz[lane]) : -INFINITY;
+    zm = wave_max_f64(zm);
+    const double w = lane < n ? exp(static_cast<double>(s.sz[lane]) - zm) : 0.0;
+    const double ws = wave_sum_f64(w);
+    if (!live[j]) continue;
+    int32_t* orow = p.topk_idx + static_cast<size_t>(t[j]) * k;
+    float* grow = p.topk_gate + static_cast<size_t>(t[j]) * k;
+    if (lane < n) {
+      const int slot = slot_of(lane, n, s.sk, s.se);
+      const int e = s.se[lane];
+      orow[slot] = e;
+      grow[slot] = static_cast<float>(w / ws);
+      atomicOr(&routed[e >> 5], 1u << (e & 31));
+    } else if (lane < k) {
+      orow[lane] = -1;  // fewer eligible experts than k (an invalid tree has none)
+      grow[lane] = 0.0f;
+    }
   }
-  const int n = wave_topk_compact<EPL>(key, k, lane, sk, se, [&](int pos, int i) { sz[pos] = zv[i]; });
-  // gates: softmax over the selected logits, fp64
-  double zm = lane < n ? static_cast<double>(sz[lane]) : -INFINITY;
-  zm = wave_max_f64(zm);
-  const double w = lane < n ? exp(static_cast<double>(sz[lane]) - zm) : 0.0;
-  const double ws = wave_sum_f64(w);
-  int32_t* orow = p.topk_idx + static_cast<size_t>(t) * k;
-  float* grow = p.topk_gate + static_cast<size_t>(t) * k;
-  if (lane < n) {
-    const int slot = slot_of(lane, n, sk, se);
-    const int e = se[lane];
-    orow[slot] = e;
-    grow[slot] = static_cast<float>(w / ws);
-    atomicOr(&routed[e >> 5], 1u << (e & 31));
-  } else if (lane < k) {
-    orow[lane] = -1;  // fewer eligible experts than k (an invalid tree has none)
-    grow[lane] = 0.0f;
+  wave_lds_sync();  // the scratch is reused by the wave's next nodes
+}
+
+// Number of list entries j2 < n ordered before entry j of value vj: larger
+// (kDesc) or smaller values first, equal values by position.  Reads eight
+// broadcast values per step; entries past n (stale, never beyond the
+// kMaxExperts-entry list) are masked out.
+template <bool kDesc>
+__device__ __forceinline__ int count_before(const double* v, int n, double vj, int j) {
+  int r = 0;
+  for (int j0 = 0; j0 < n; j0 += 8) {
+    const double2 a = *reinterpret_cast<const double2*>(v + j0);
+    const double2 b = *reinterpret_cast<const double2*>(v + j0 + 2);
+    const double2 c = *reinterpret_cast<const double2*>(v + j0 + 4);
+    const double2 d = *reinterpret_cast<const double2*>(v + j0 + 6);
+    const double vv[8] = {a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const bool beats = kDesc ? (vv[q] > vj) : (vv[q] < vj);
+      r += static_cast<int>((j0 + q < n) & (beats | ((vv[q] == vj) & (j0 + q < j))));
+    }
   }
-  wave_lds_sync();  // the scratch is reused by the wave's next node
+  return r;
 }
 
 // ---------------------------------------------------------------------------
@@ -349,30 +455,33 @@ __device__ void eligible_set_wave(SelShared& sh, int mode, int E, int k, int bud
     ner = take;
   }
   // S = A u first `take` of R in (u desc, index asc) order: members with u > 0
-  // (compacted in index order) ranked among themselves, then u = 0 members in
-  // index order if needed
+  // by a top-`take` search over their utilities' bit patterns (u > 0, so the
+  // bits order like the values; equal utilities go lowest index first), then
+  // u = 0 members in index order if needed
+  uint64_t ukey[1][EPL];
   int np = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const bool f = inR[i] && u[i] > 0.0;
-    const uint64_t m = __ballot(f);
-    if (f) {
-      const int pos = np + popc64(m & lanes_below(lane));
-      sh.plist[pos] = lane + kWave * i;
-      sh.pval[pos] = u[i];
-    }
-    np += popc64(m);
+    ukey[0][i] = f ? static_cast<uint64_t>(__double_as_longlong(u[i])) : 0ull;
+    np += popc64(__ballot(f));
   }
-  wave_lds_sync();
-  for (int j0 = 0; j0 < np; j0 += kWave) {
-    const int j = j0 + lane;
-    const double vj = j < np ? sh.pval[j] : 0.0;
-    int r = 0;
-    for (int j2 = 0; j2 < np; ++j2) {
-      const double v2 = sh.pval[j2];
-      r += static_cast<int>((v2 > vj) | ((v2 == vj) & (j2 < j)));
+  if (take > 0 && np > 0) {
+    uint64_t thr[1];
+    kth_largest<EPL, 1>(ukey, take, thr);
+    int greater = 0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) greater += popc64(__ballot(ukey[0][i] > thr[0]));
+    const int need = take - greater;
+    const uint64_t below = lanes_below(lane);
+    int eq_before = 0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const bool eq = ukey[0][i] == thr[0] && ukey[0][i] != 0ull;
+      const uint64_t eqm = __ballot(eq);
+      if ((ukey[0][i] > thr[0]) | (eq & ((eq_before + popc64(eqm & below)) < need))) sh.inS[lane + kWave * i] = 1;
+      eq_before += popc64(eqm);
     }
-    if (j < np && r < take) sh.inS[sh.plist[j]] = 1;
   }
   if (take > np) {
     int base = 0;
@@ -413,11 +522,7 @@ __device__ void eligible_set_wave(SelShared& sh, int mode, int E, int k, int bud
     for (int j0 = 0; j0 < nC; j0 += kWave) {
       const int j = j0 + lane;
       const double vj = j < nC ? sh.pval[j] : 0.0;
-      int r = 0;
-      for (int j2 = 0; j2 < nC; ++j2) {
-        const double v2 = sh.pval[j2];
-        r += static_cast<int>((v2 < vj) | ((v2 == vj) & (j2 < j)));
-      }
+      const int r = count_before<false>(sh.pval, nC, vj, j);
       if (j < nC) {
         const int e = sh.plist[j];
         sh.rankv[e] = r;
@@ -461,20 +566,19 @@ __device__ void eligible_set_wave(SelShared& sh, int mode, int E, int k, int bud
 }
 
 // ---------------------------------------------------------------------------
-// eligible set of one tree
+// tree stage of one tree, in phases
 // ---------------------------------------------------------------------------
-template <int EPL>
-__global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeOffsets offs) {
-  __shared__ SelShared sh;
-  const int tid = threadIdx.x;
-  const int wave = wave_id(), lane = lane_id();
-  const int b = blockIdx.x;
-  const int t_begin = offs.o[b];
-  const int Tb = offs.o[b + 1] - t_begin;
-  const int E = p.E, k = p.k;
-  const bool has_mask = p.resident != nullptr;
+struct TreeCtx {
+  int b, t_begin, Tb, tid, wave, lane;
+  int my_d;     // depth of node tid (tid < Tb)
+  float my_p;   // its commitment probability
+};
 
-  // ---------------- P1: inputs, tree checks, N_d ----------------
+// P1: LDS state, the node inputs (thread tid reads node tid), tree checks and
+// depth counts N_d.  The caller synchronizes before tree_code.
+__device__ __forceinline__ void tree_p1(SelShared& sh, const SelectParams& p, TreeCtx& c) {
+  const int tid = c.tid, Tb = c.Tb, t_begin = c.t_begin, E = p.E;
+  const bool has_mask = p.resident != nullptr;
   if (tid == 0) {
     sh.code = Tb > 0 ? 0x7fffffff : CODE_EMPTY;
     sh.n_anchor = sh.n_unat = sh.n_R = sh.n_pos = sh.n_S = sh.n_C = sh.n_Sp = sh.n_routed = 0;
@@ -489,23 +593,14 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
     sh.score[e] = 0.0;
     sh.resident[e] = (e < E) ? (has_mask ? (p.resident[e] != 0) : 1) : 0;
   }
-  if (tid < kRoutedWords) p.ws_routed[b * kRoutedWords + tid] = 0u;
-  // the first utility chunk's natural top-k entries, loaded now so their
-  // latency overlaps the node loads below
-  const int chunk = kDenseDoubles / E;  // >= 8 for E <= 512
-  int pf_e = 0;
-  double pf_r = 0.0;
-  if (tid < min(chunk, Tb) * k) {
-    const size_t gi = static_cast<size_t>(t_begin) * k + tid;
-    pf_e = p.ws_kidx[gi];
-    pf_r = p.ws_r[gi];
-  }
-  int my_d = -1;
-  float my_p = 0.0f;
+  c.my_d = -1;
+  c.my_p = 0.0f;
   if (tid < Tb) {
     const int t = t_begin + tid;
-    my_d = p.depth[t];
-    my_p = p.prob[t];
+    c.my_d = p.depth[t];
+    c.my_p = p.prob[t];
+    const int my_d = c.my_d;
+    const float my_p = c.my_p;
     const int par = p.parent != nullptr ? p.parent[t] : 0;
     const int par_d = (p.parent != nullptr && tid > 0 && par >= t_begin && par < t) ? p.depth[par] : 0;
     int code = 0;
@@ -521,29 +616,38 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
     if (code) atomicMin(&sh.code, code);
     if (my_d >= 0 && my_d < Tb) atomicAdd(&sh.Nd[my_d], 1);
   }
-  __syncthreads();
-  const int code = (sh.code == 0x7fffffff) ? 0 : sh.code;
+}
 
-  if (code != 0) {
-    // invalid tree: an empty eligible set, so its nodes get no routing
-    for (int e = tid; e < E; e += kSelThreads) p.eligible[static_cast<size_t>(b) * E + e] = 0;
-    if (p.stats != nullptr && tid < kNumStats) {
-      int v = 0;
-      if (tid == 0) v = Tb;
-      if (tid == 8) v = code;
-      p.stats[b * kNumStats + tid] = v;
-    }
-    return;
+__device__ __forceinline__ int tree_code(const SelShared& sh) { return sh.code == 0x7fffffff ? 0 : sh.code; }
+
+// invalid tree: an empty eligible set, so its nodes get no routing
+__device__ __forceinline__ void tree_invalid(const SelectParams& p, const TreeCtx& c, int code) {
+  for (int e = c.tid; e < p.E; e += kSelThreads) p.eligible[static_cast<size_t>(c.b) * p.E + e] = 0;
+  if (p.stats != nullptr && c.tid < kNumStats) {
+    int v = 0;
+    if (c.tid == 0) v = c.Tb;
+    if (c.tid == 8) v = code;
+    p.stats[c.b * kNumStats + c.tid] = v;
   }
-  // alpha_t = p_t^beta / sqrt(N_{d_t})   (Eq. 3)
-  if (tid < Tb) {
-    const double pd = static_cast<double>(my_p);
+}
+
+// alpha_t = p_t^beta / sqrt(N_{d_t})   (Eq. 3); the caller synchronizes
+__device__ __forceinline__ void tree_alpha(SelShared& sh, const SelectParams& p, const TreeCtx& c) {
+  if (c.tid < c.Tb) {
+    const double pd = static_cast<double>(c.my_p);
     const double pb = p.beta == 0.5 ? sqrt(pd) : (p.beta == 1.0 ? pd : pow(pd, p.beta));
-    sh.alpha[tid] = pb / sqrt(static_cast<double>(sh.Nd[my_d]));
+    sh.alpha[c.tid] = pb / sqrt(static_cast<double>(sh.Nd[c.my_d]));
   }
-  __syncthreads();
+}
 
-  // ---------------- P3: votes, anchor, utility in node order ----------------
+// P3: votes, anchor and the utility in node order.  kidx / rr hold the
+// tree's natural entries, node tl's slot j at tl * k + j.  With kPre the
+// first chunk's entry tid was loaded beforehand into (pf_e, pf_r).
+template <bool kPre>
+__device__ __forceinline__ void tree_p3(SelShared& sh, const SelectParams& p, const TreeCtx& c,
+                                        const int32_t* kidx, const double* rr, int pf_e, double pf_r) {
+  const int tid = c.tid, lane = c.lane, Tb = c.Tb, E = p.E, k = p.k;
+  const int chunk = kDenseDoubles / E;  // >= 8 for E <= 512
   double u_acc = 0.0;
   for (int c0 = 0; c0 < Tb; c0 += chunk) {
     const int cn = min(chunk, Tb - c0);
@@ -551,10 +655,10 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
     __syncthreads();
     for (int i = tid; i < cn * k; i += kSelThreads) {
       const int tl = c0 + i / k;
-      const size_t gi = static_cast<size_t>(t_begin + tl) * k + (i % k);
-      const bool pf = c0 == 0 && i == tid;  // loaded at the start
-      const int e = pf ? pf_e : p.ws_kidx[gi];
-      sh.dense[(tl - c0) * E + e] = sh.alpha[tl] * (pf ? pf_r : p.ws_r[gi]);
+      const int gi = c0 * k + i;
+      const bool pf = kPre && c0 == 0 && i == tid;  // loaded at the start
+      const int e = pf ? pf_e : kidx[gi];
+      sh.dense[(tl - c0) * E + e] = sh.alpha[tl] * (pf ? pf_r : rr[gi]);
       atomicAdd(&sh.votes[e], 1);
       if (tl == 0) sh.anchor[e] = 1;  // the root is the tree's only depth-0 node
     }
@@ -565,28 +669,30 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
     }
     __syncthreads();
   }
-  {
-    const bool in_e = tid < E;
-    const bool anc = in_e && sh.anchor[tid];
-    if (in_e) {
-      sh.u[tid] = u_acc;
-      sh.inR[tid] = !anc;
-    }
-    wg_count(anc, &sh.n_anchor, lane);
-    wg_count(in_e && sh.votes[tid] > 0, &sh.n_unat, lane);
-    wg_count(in_e && !anc, &sh.n_R, lane);
-    wg_count(in_e && !anc && u_acc > 0.0, &sh.n_pos, lane);
+  const bool in_e = tid < E;
+  const bool anc = in_e && sh.anchor[tid];
+  if (in_e) {
+    sh.u[tid] = u_acc;
+    sh.inR[tid] = !anc;
   }
-  __syncthreads();
+  wg_count(anc, &sh.n_anchor, lane);
+  wg_count(in_e && sh.votes[tid] > 0, &sh.n_unat, lane);
+  wg_count(in_e && !anc, &sh.n_R, lane);
+  wg_count(in_e && !anc && u_acc > 0.0, &sh.n_pos, lane);
+}
 
-  // ---------------- P4: eligible set ----------------
+// P4 and the tree's outputs: S' into sh.inSp and eligible[b], statistics
+// (routed experts left 0).  Ends synchronized.
+template <int EPL>
+__device__ __forceinline__ void tree_p4(SelShared& sh, const SelectParams& p, const TreeCtx& c) {
+  const int tid = c.tid, wave = c.wave, lane = c.lane, Tb = c.Tb, t_begin = c.t_begin, E = p.E, k = p.k;
   const int mode = p.mode;
   const int kmin = min(k, E);
   const int bud = p.budget < kmin ? kmin : (p.budget > E ? E : p.budget);
 
   if (mode == MODE_SELF || mode == MODE_FIXED) {
     // Eq. 6, S, |S|, a(S) and the Eq. 7 pruning in one wave
-    if (wave == 0) eligible_set_wave<EPL>(sh, mode, E, k, bud, p.removal_cap, has_mask, lane);
+    if (wave == 0) eligible_set_wave<EPL>(sh, mode, E, k, bud, p.removal_cap, p.resident != nullptr, lane);
     __syncthreads();
   } else {
     if (mode == MODE_MOESPEC || mode == MODE_COUNT) {
@@ -627,12 +733,11 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
   }
   __syncthreads();
 
-  // ---------------- outputs ----------------
-  if (tid < E) p.eligible[static_cast<size_t>(b) * E + tid] = sh.inSp[tid];
+  if (tid < E) p.eligible[static_cast<size_t>(c.b) * E + tid] = sh.inSp[tid];
   wg_count(tid < E && sh.inSp[tid], &sh.n_Sp, lane);
   __syncthreads();
   if (p.stats != nullptr && tid == 0) {
-    int32_t* st = p.stats + b * kNumStats;
+    int32_t* st = p.stats + c.b * kNumStats;
     st[0] = Tb;
     st[1] = sh.n_anchor;
     st[2] = sh.n_er;
@@ -642,8 +747,54 @@ __global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeO
     st[6] = sh.budget_a;
     st[7] = sh.m_star;
     st[8] = 0;
-    st[9] = 0;  // routed experts, counted by restricted_kernel
+    st[9] = 0;  // routed experts, counted by the restricted stage
   }
+}
+
+__device__ __forceinline__ TreeCtx tree_ctx(const TreeOffsets& offs, int b) {
+  TreeCtx c;
+  c.b = b;
+  c.t_begin = offs.o[b];
+  c.Tb = offs.o[b + 1] - c.t_begin;
+  c.tid = threadIdx.x;
+  c.wave = wave_id();
+  c.lane = lane_id();
+  c.my_d = -1;
+  c.my_p = 0.0f;
+  return c;
+}
+
+// ---------------------------------------------------------------------------
+// eligible set of one tree
+// ---------------------------------------------------------------------------
+template <int EPL>
+__global__ __launch_bounds__(kSelThreads) void tree_kernel(SelectParams p, TreeOffsets offs) {
+  __shared__ SelShared sh;
+  TreeCtx c = tree_ctx(offs, blockIdx.x);
+  const int tid = c.tid, k = p.k;
+  if (tid < kRoutedWords) p.ws_routed[c.b * kRoutedWords + tid] = 0u;
+  // the first utility chunk's natural top-k entries, loaded now so their
+  // latency overlaps the node loads of P1
+  const int32_t* kidx = p.ws_kidx + static_cast<size_t>(c.t_begin) * k;
+  const double* rr = p.ws_r + static_cast<size_t>(c.t_begin) * k;
+  int pf_e = 0;
+  double pf_r = 0.0;
+  if (tid < min(kDenseDoubles / p.E, c.Tb) * k) {
+    pf_e = kidx[tid];
+    pf_r = rr[tid];
+  }
+  tree_p1(sh, p, c);
+  __syncthreads();
+  const int code = tree_code(sh);
+  if (code != 0) {
+    tree_invalid(p, c, code);
+    return;
+  }
+  tree_alpha(sh, p, c);
+  __syncthreads();
+  tree_p3<true>(sh, p, c, kidx, rr, pf_e, pf_r);
+  __syncthreads();
+  tree_p4<EPL>(sh, p, c);
 }
 
 // ---------------------------------------------------------------------------
@@ -673,8 +824,12 @@ __global__ __launch_bounds__(kNodeWaves * kWave) void restricted_kernel(SelectPa
     }
     b = lo;
     wave_lds_sync();
-    restricted_node<EPL>(p, t, p.eligible + static_cast<size_t>(b) * p.E, lane, ns.sk[wave], ns.se[wave],
-                         ns.sz[wave], routed[wave]);
+    const int tt[1] = {t};
+    const bool live[1] = {true};
+    float zv[1][EPL];
+    load_row<EPL>(p.logits + static_cast<size_t>(t) * p.E, p.E, lane, zv[0]);
+    NodeSlot* const sl[1] = {&ns.s[wave]};
+    restricted_nodes<EPL, 1>(p, tt, live, zv, p.eligible + static_cast<size_t>(b) * p.E, lane, sl, routed[wave]);
   }
   if (lane == 0) tree_of[wave] = b;
   if (p.stats == nullptr) return;
