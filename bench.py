@@ -303,7 +303,7 @@ def main():
                    "rho": args.rho, "weight_sets": n_sets, "blocks": args.blocks,
                    "routed_experts": round(main_m["routed"], 2), "eligible": round(main_m["sprime"], 2),
                    "natural_union": round(main_m["unat"], 2)},
-        "roofline": {"bound": "hbm", "kernel": "acceptmoe_moe_forward (gate_up with in-LDS dispatch + down with in-LDS combine)",
+        "roofline": {"bound": "hbm", "kernel": "acceptmoe_moe_forward (gate_up with per-item dispatch + down with in-LDS combine)",
                      "achieved": round(main_m["fwd_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(frac, 4),
                      "traffic": (None if measured_traffic() is None

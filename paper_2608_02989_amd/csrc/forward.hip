@@ -274,7 +274,34 @@ __device__ __forceinline__ void self_dispatch(const ForwardParams& p, SelfDispat
   __syncthreads();
 }
 
-// workgroup 0: CSR, active list and down items to the workspace
+// Per-item dispatch of the gate/up pass: a workgroup needs only the expert of
+// its item (the a-th routed expert in index order, from the block's routed
+// mask), that expert's slot ids in node order, its count n_e and its first
+// CSR row o_e (the dispatched slots of lower experts) -- a few ballots over
+// the routing rows, so the weight stream starts early.
+template <int KMAX>
+struct ItemDispatch {
+  uint32_t emask[kMaxExperts / 32];  // routed experts of the block
+  int wcnt[4], wless[4];             // per wave: its tokens of e, its slots below e
+  int ent[kSelfMaxT];                // slot ids of e (one per token at most)
+  int row[kSelfMaxT][KMAX];          // routing rows, kept here rather than in registers
+  uint32_t valid[kSelfMaxT];         // their dispatched slots (load_route_row)
+};
+
+// the a-th set bit of mask[0 .. words) (a < number of set bits)
+__device__ __forceinline__ int nth_set_bit(const uint32_t* mask, int words, int a) {
+  int w = 0;
+  for (; w + 1 < words; ++w) {
+    const int c = __popc(mask[w]);
+    if (a < c) break;
+    a -= c;
+  }
+  uint32_t m = mask[w];
+  for (int i = 0; i < a; ++i) m &= m - 1u;  // drop the a lowest set bits
+  return 32 * w + __builtin_ctz(m);
+}
+
+// CSR, active list and down items to the workspace
 __device__ __forceinline__ void publish_dispatch(const ForwardParams& p, const SelfDispatch& sd, int tid) {
   const int E = p.E;
   for (int e = tid; e <= E; e += 256) {
@@ -582,8 +609,9 @@ struct ProjShape {
   static constexpr int kTilesPerWG = 4 * NTW / KS;
 };
 
+// ent_e: the n_e slot ids of expert e in node order; o_e: its first row in act
 template <class P, Proj F, int MT, int NTW, int KS>
-__device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* ent, int e, int tile_base, int n_e,
+__device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* ent_e, int e, int tile_base, int n_e,
                                          int o_e, int m0, floatx4 (*red)[kWave][4], uint4* xs) {
   static_assert(F != Proj::GateUp || NTW == 2, "the packed gate/up layout holds tile pairs");
   constexpr int NB = ProjShape<F, NTW, KS>::kNB;
@@ -599,11 +627,11 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* 
   const uint4* x[MT];
   if (F == Proj::GateUp) {
     const uint4* hid = static_cast<const uint4*>(p.hidden);
-    const int tok0 = ent[o_e] / p.k;  // rows past n_e read a valid row; their outputs are dropped
+    const int tok0 = ent_e[0] / p.k;  // rows past n_e read a valid row; their outputs are dropped
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int m = m0 + mt * 16 + r;
-      const int tok = m < n_e ? ent[o_e + m] / p.k : tok0;
+      const int tok = m < n_e ? ent_e[m] / p.k : tok0;
       x[mt] = hid + static_cast<size_t>(tok) * rowq + g;
     }
   } else {
@@ -686,7 +714,7 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* 
               else
                 static_cast<float*>(p.act)[idx] = v;
             } else {
-              const int s = ent[o_e + m];
+              const int s = ent_e[m];
               p.ys[static_cast<size_t>(s) * p.H + tile * 16 + r] = p.topk_gate[s] * acc[j][mt][i];
             }
           }
@@ -696,12 +724,14 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* 
   }
 }
 
-template <bool kSelf>
-struct SelfDispatchSlot {
+// the full CSR is built only by the publishing workgroup, after its items
+template <bool kSelf, int KMAX>
+union SelfDispatchSlot {
   SelfDispatch sd;
+  ItemDispatch<KMAX> id;
 };
-template <>
-struct SelfDispatchSlot<false> {
+template <int KMAX>
+union SelfDispatchSlot<false, KMAX> {
   int unused;
 };
 
@@ -709,17 +739,21 @@ struct SelfDispatchSlot<false> {
 // Without kSelf: grid.x = cap_experts * wg_per_expert, one item per
 // workgroup, reading dispatch_kernel's CSR.  kSelf (gate/up pass, blocks of up
 // to kSelfMaxT tokens): a grid no larger than what is resident at once (so no
-// workgroup waits for a slot and repeats the dispatch) builds the dispatch in
-// LDS once per workgroup and takes items blockIdx.x, blockIdx.x + gridDim.x,
-// ...  (A device-wide work counter was tried: every workgroup's first atomic
+// workgroup waits for a slot) takes items blockIdx.x, blockIdx.x + gridDim.x,
+// ..., each with its own per-item dispatch; the last workgroup, which has the
+// fewest items, builds the full CSR afterwards and publishes it for the down
+// pass.  (A device-wide work counter was tried: every workgroup's first atomic
 // hits the same address at once and the serialized atomics cost more than
 // the balance gained.)
 
+// Occupancy floor: three workgroups per CU for up to two M-tiles, two for
+// more (the register budget the streaming loop is tuned to).
 template <class P, Proj F, int MTMAX, int NTW, int KS, bool kSelf, int KMAX>
-__global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MTMAX <= 2 ? 3 : 2))) void ffn_kernel(
+    ForwardParams p) {
   __shared__ floatx4 red[KS > 1 ? 4 : 1][kWave][4];
   __shared__ uint4 xs[KS == 1 ? shared_a_pieces<MTMAX>() * kWave : 1];
-  __shared__ SelfDispatchSlot<kSelf> sds;
+  __shared__ SelfDispatchSlot<kSelf, KMAX> sds;
   constexpr int tpw = ProjShape<F, NTW, KS>::kTilesPerWG;
   const int ntiles = (F == Proj::GateUp ? p.I : p.H) / 16;
   const int wg_per_expert = (ntiles + tpw - 1) / tpw;
@@ -731,29 +765,89 @@ __global__ __launch_bounds__(256) void ffn_kernel(ForwardParams p) {
          i += static_cast<size_t>(gridDim.x) * blockDim.x)
       o4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  auto run_item = [&](int item, const int* active, const int* cnt, const int* off, const int32_t* ent) {
-    const int a = item / wg_per_expert;
-    const int tile_base = (item % wg_per_expert) * tpw;
-    const int e = active[a];
-    const int n_e = cnt[e];
-    const int o_e = off[e];
+  auto run_expert = [&](int tile_base, int e, int n_e, int o_e, const int32_t* ent_e) {
     for (int m0 = 0; m0 < n_e; m0 += 16 * MTMAX) {
       const int nmt = min(MTMAX, (n_e - m0 + 15) / 16);
-      if (nmt == 1) ffn_pass<P, F, 1, NTW, KS>(p, ent, e, tile_base, n_e, o_e, m0, red, xs);
-      else if (MTMAX >= 2 && nmt == 2) ffn_pass<P, F, (MTMAX >= 2 ? 2 : 1), NTW, KS>(p, ent, e, tile_base, n_e, o_e, m0, red, xs);
-      else if (MTMAX >= 3 && nmt == 3) ffn_pass<P, F, (MTMAX >= 3 ? 3 : 1), NTW, KS>(p, ent, e, tile_base, n_e, o_e, m0, red, xs);
-      else ffn_pass<P, F, MTMAX, NTW, KS>(p, ent, e, tile_base, n_e, o_e, m0, red, xs);
+      if (nmt == 1) ffn_pass<P, F, 1, NTW, KS>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
+      else if (MTMAX >= 2 && nmt == 2) ffn_pass<P, F, (MTMAX >= 2 ? 2 : 1), NTW, KS>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
+      else if (MTMAX >= 3 && nmt == 3) ffn_pass<P, F, (MTMAX >= 3 ? 3 : 1), NTW, KS>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
+      else ffn_pass<P, F, MTMAX, NTW, KS>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
     }
   };
   if constexpr (kSelf) {
-    SelfDispatch& sd = sds.sd;
-    self_dispatch<KMAX>(p, sd, threadIdx.x);
-    if (blockIdx.x == 0) publish_dispatch(p, sd, threadIdx.x);
-    const int n_items = sd.nact * wg_per_expert;
-    for (int item = blockIdx.x; item < n_items; item += gridDim.x) run_item(item, sd.active, sd.cnt, sd.off, sd.ent);
+    ItemDispatch<KMAX>& id = sds.id;
+    const int tid = threadIdx.x, wave = wave_id(), lane = lane_id();
+    const int T = p.T, k = p.k, E = p.E, words = (E + 31) / 32;
+    if (tid < kMaxExperts / 32) id.emask[tid] = 0u;
+    {
+      int ev[KMAX];
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j) ev[j] = -1;
+      uint32_t valid = 0u;
+      if (tid < T) {
+        valid = load_route_row<KMAX>(p.topk_idx + static_cast<size_t>(tid) * k, k, E, ev);
+#pragma unroll
+        for (int j = 0; j < KMAX; ++j) id.row[tid][j] = ev[j];
+        id.valid[tid] = valid;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j)
+        if (valid & (1u << j)) atomicOr(&id.emask[ev[j] >> 5], 1u << (ev[j] & 31));
+    }
+    __syncthreads();
+    // workgroup-uniform values go to scalar registers (the streaming loop
+    // needs every vector register it can get)
+    int nact = 0;
+    for (int w = 0; w < words; ++w) nact += __popc(id.emask[w]);
+    nact = __builtin_amdgcn_readfirstlane(nact);
+    const int n_items = nact * wg_per_expert;
+    for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+      const int e = __builtin_amdgcn_readfirstlane(nth_set_bit(id.emask, words, item / wg_per_expert));
+      // this thread's token: its slot of e, and its slots of lower experts
+      int slot = -1, less = 0;
+      if (tid < T) {
+        const uint32_t valid = id.valid[tid];
+#pragma unroll
+        for (int j = 0; j < KMAX; ++j) {
+          const int ej = id.row[tid][j];
+          if (valid & (1u << j)) {
+            slot = ej == e ? static_cast<int>(tid) * k + j : slot;
+            less += ej < e ? 1 : 0;
+          }
+        }
+      }
+      const uint64_t hm = __ballot(slot >= 0);
+      const int wless = wave_sum_i32(less);
+      __syncthreads();  // the previous item's list is no longer read
+      if (lane == 0) {
+        id.wcnt[wave] = popc64(hm);
+        id.wless[wave] = wless;
+      }
+      __syncthreads();
+      int before = 0, n_e = 0, o_e = 0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        before += w < wave ? id.wcnt[w] : 0;
+        n_e += id.wcnt[w];
+        o_e += id.wless[w];
+      }
+      if (slot >= 0) id.ent[before + popc64(hm & lanes_below(lane))] = slot;
+      __syncthreads();
+      run_expert((item % wg_per_expert) * tpw, e, __builtin_amdgcn_readfirstlane(n_e),
+                 __builtin_amdgcn_readfirstlane(o_e), id.ent);
+    }
+    if (blockIdx.x == gridDim.x - 1) {
+      __syncthreads();  // the per-item state shares this LDS
+      SelfDispatch& sd = sds.sd;
+      self_dispatch<KMAX>(p, sd, tid);
+      publish_dispatch(p, sd, tid);
+    }
   } else {
     if (static_cast<int>(blockIdx.x) >= *p.n_active * wg_per_expert) return;
-    run_item(blockIdx.x, p.active, p.cnt, p.off, p.ent_slot);
+    const int a = blockIdx.x / wg_per_expert;
+    const int e = p.active[a];
+    run_expert((blockIdx.x % wg_per_expert) * tpw, e, p.cnt[e], p.off[e], p.ent_slot + p.off[e]);
   }
 }
 
