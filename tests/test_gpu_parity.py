@@ -300,6 +300,33 @@ def test_forward_parity_ragged_and_hot_expert(gpu, dtype, T):
     assert np.all(got[6] == 0.0)
 
 
+# no token routed at all (every entry invalid): no expert is streamed and the
+# output is zero; then a routed call on the same workspace (no stale dispatch)
+@pytest.mark.parametrize("T", [32, 300])
+def test_forward_no_routed_expert(gpu, T):
+    cfg = W.LayerConfig("unrouted", 93 + T, "bf16", T=T, B=1, H=256, E=20, k=4, I=96, depth_max=6,
+                        commit_rule="depth_sibling", hidden_std=1.0)
+    rng = np.random.default_rng(T + 17)
+    h32 = rng.standard_normal((T, cfg.H)).astype(np.float32)
+    hdev, h64 = hidden_for(cfg, h32)
+    wg, wu, wd = W.expert_weights_torch(cfg, 0, DEV)
+    pgu, pd = ops.pack_gate_up_weights(wg, wu), ops.pack_expert_weights(wd)
+    ws = ops.forward_workspace(T, cfg.H, cfg.I, cfg.E, cfg.k, torch.bfloat16, DEV)
+    out = torch.full((T, cfg.H), 7.0, dtype=torch.float32, device=DEV)
+    idx = np.full((T, cfg.k), -1, np.int32)
+    idx[::3, 1] = cfg.E + 5                         # out of range: skipped as well
+    gate = rng.random((T, cfg.k)).astype(np.float32)
+    say(f"forward no routed expert T={T}")
+    ops.moe_forward(to_dev_hidden(cfg, hdev), pgu, pd, i32(idx), f32(gate), out=out, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(out).item() == 0
+    idx2 = np.stack([rng.permutation(cfg.E)[:cfg.k] for _ in range(T)]).astype(np.int32)
+    ops.moe_forward(to_dev_hidden(cfg, hdev), pgu, pd, i32(idx2), f32(gate), out=out, workspace=ws)
+    torch.cuda.synchronize()
+    ref = O.moe_forward_grouped(h64, HostExperts(wg), HostExperts(wu), HostExperts(wd), idx2, gate, cfg.dtype)
+    assert normwise_rel(out.cpu().numpy(), ref) <= FWD_TOL[cfg.dtype]
+
+
 # forward path limits: k > 8 in the in-LDS dispatch, exactly 256 tokens / 2048
 # slots (largest column-tile block), 257 tokens (per-slot pass), E = 48
 @pytest.mark.parametrize("T,k,E,dtype", [(40, 32, 64, "bf16"), (37, 12, 48, "f32"), (256, 8, 64, "bf16"),
