@@ -14,14 +14,16 @@
 // Three launches: natural_kernel and restricted_kernel put one wave on each
 // node and spread the nodes over many CUs; tree_kernel runs one 1024-thread
 // workgroup per tree between them.  The per-node top-k is bound by
-// instruction issue (a 32-step ballot search, fp64 exponentials): a block's
-// nodes on one CU queue behind each other on its four SIMDs, which costs more
-// than the two launches saved by running everything in one workgroup.
+// instruction issue (a ballot search over the key bits, fp64 exponentials):
+// a block's nodes on one CU queue behind each other on its four SIMDs, which
+// costs more than the two launches saved by running everything in one
+// workgroup.
 //
-// Top-k is a wave-wide radix select on order-preserving 32-bit keys: the k-th
-// largest key is found bit by bit with ballots, keys above it are taken,
-// equal keys are taken lowest expert index first.  This matches the rank
-// definition "fewer than k experts beat e" exactly, ties included.
+// Top-k is a wave-wide radix select on order-preserving keys: the k-th
+// largest key is found bit by bit with ballots (stopping once exactly k keys
+// remain above the prefix), keys above it are taken, equal keys are taken
+// lowest expert index first.  This matches the rank definition "fewer than k
+// experts beat e" exactly, ties included.
 #include "common.hpp"
 #include "launch.hpp"
 
