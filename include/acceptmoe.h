@@ -88,7 +88,8 @@ extern "C" {
  * [E, H] (nn.Linear orientation, row-major) into the layout acceptmoe_route
  * reads.  Each weight w becomes three bf16 values (round to nearest even)
  * hi = bf16(w), mid = bf16(w - hi), lo = bf16(w - hi - mid), whose sum is w
- * exactly for |w| above about 1e-33.  Rows are padded with zeros to a
+ * exactly for 1e-33 < |w| < 3.39e38 (the largest bf16; beyond it hi is
+ * infinite).  Rows are padded with zeros to a
  * multiple of 16 and columns to a multiple of 32; then for every 16-row tile
  * et, every 32-column chunk c and every plane p (0 hi, 1 mid, 2 lo) a
  * fragment of 64 lanes x 16 B follows, lane L holding plane p of row

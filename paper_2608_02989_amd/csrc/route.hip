@@ -4,8 +4,9 @@
 //
 // The fp32 router matrix is stored as three bf16 planes, hi = bf16(w),
 // mid = bf16(w - hi), lo = bf16(w - hi - mid), whose sum is w exactly for
-// every |w| above about 1e-33 (below, the remainders leave the normal range
-// and the loss is under 2^-125 per weight).  A bf16 hidden state then takes
+// every |w| between about 1e-33 and 3.39e38 (below, the remainders leave the
+// normal range and the loss is under 2^-125 per weight; above, the largest
+// bf16 is exceeded and hi is infinite).  A bf16 hidden state then takes
 // the bf16 MFMA (v_mfma_f32_16x16x32_bf16) three times per chunk, once per
 // plane, with exact products and fp32 accumulation: three instructions that
 // together run about five times faster than the fp32 MFMA they replace,
