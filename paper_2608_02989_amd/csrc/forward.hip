@@ -1083,7 +1083,12 @@ hipError_t launch_down_rows(const ForwardParams& p, int cap, hipStream_t stream)
 
 // Column-tile down pass shape: I split in two when that keeps the grid near
 // 256 workgroups, two column tiles per workgroup for wide H, k-steps per
-// pipeline stage dividing the part of I.
+// pipeline stage: the largest of 12, 8, 6, 4, 2, 1 dividing the part of I,
+// at most 12 with one column tile (two stages in flight then fit the
+// registers of one 8-wave workgroup per CU, and the deeper stages keep more
+// bytes in flight: 12 vs 4 k-steps measured 0.6 us faster at H = 2048,
+// I = 768) and at most 4 with two (whose stages already carry twice the
+// weight bytes; 8 measured slower at H = 4096, I = 1536).
 struct ColShape {
   int ksplit, ku, nb;
 };
@@ -1095,7 +1100,13 @@ ColShape col_shape(int H, int I, int is_bf16) {
   c.nb = (ntiles >= 256 && ntiles % 2 == 0) ? 2 : 1;
   c.ksplit = (ntiles / c.nb <= 128 && KC % 2 == 0) ? 2 : 1;
   const int len = KC / c.ksplit;
-  c.ku = len % 4 == 0 ? 4 : (len % 2 == 0 ? 2 : 1);
+  c.ku = 1;
+  for (const int u : {12, 8, 6, 4, 2}) {
+    if (len % u == 0 && u <= (c.nb == 1 ? 12 : 4)) {
+      c.ku = u;
+      break;
+    }
+  }
   return c;
 }
 
@@ -1110,6 +1121,14 @@ template <class P, int NB>
 hipError_t launch_down_col_nb(const ForwardParams& p, const ColShape& c, hipStream_t stream) {
   const dim3 grid((p.H / 16 / NB) * c.ksplit);
   constexpr int threads = kColLanes / NB * kWave;
+  if constexpr (NB == 1) {  // deeper stages only with one column tile (col_shape)
+    if (c.ku == 12 || c.ku == 8 || c.ku == 6) {
+      if (c.ku == 12) down_col_kernel<P, 12, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+      else if (c.ku == 8) down_col_kernel<P, 8, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+      else down_col_kernel<P, 6, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+      return hipGetLastError();
+    }
+  }
   if (c.ku == 4) down_col_kernel<P, 4, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
   else if (c.ku == 2) down_col_kernel<P, 2, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
   else down_col_kernel<P, 1, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
