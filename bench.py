@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--phys-layers", type=int, default=4, help="layers of the physical (copying) offload run")
     ap.add_argument("--estimate", action="store_true",
                     help="offline commitment estimator report (p_hat from synthetic traces, tree and chain blocks)")
+    ap.add_argument("--tp-share", type=int, default=1, metavar="G",
+                    help="time one GPU's share of a G-way tensor-parallel split over I: the same routing "
+                         "(router, hidden states and trees as the full layer), experts with I/G rows")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="only run a plain device copy of MB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -127,6 +130,15 @@ def main():
     if cfg.layers > 1:
         stack_report(args, cfg)
         return
+    full_I = cfg.I
+    if args.tp_share > 1:
+        # one GPU's shard: the seeds depend on the configuration id, not on I,
+        # so routing is the full layer's and only the expert weights shrink
+        G = args.tp_share
+        if cfg.I % (32 * G) != 0:
+            print(f"--tp-share {G}: I = {cfg.I} does not split into {G} multiples of 32", file=sys.stderr)
+            sys.exit(2)
+        cfg = W.LayerConfig(**{**cfg.__dict__, "I": cfg.I // G})
     Ttot = cfg.total_tokens
     ebytes = cfg.expert_bytes
     layer_bytes = cfg.E * ebytes
@@ -298,9 +310,12 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: 1 MoE layer, verify block T={Ttot} (B={cfg.B} trees), "
                                f"H={cfg.H} E={cfg.E} top-{cfg.k} I={cfg.I}, {cfg.dtype} experts, fp32 router, "
-                               f"tree-correlated hidden rho={args.rho}",
+                               f"tree-correlated hidden rho={args.rho}"
+                               + (f"; one GPU's I/{args.tp_share} shard of I={full_I} (tensor parallel over I)"
+                                  if args.tp_share > 1 else ""),
                    "T": Ttot, "B": cfg.B, "H": cfg.H, "E": cfg.E, "k": cfg.k, "I": cfg.I,
                    "rho": args.rho, "weight_sets": n_sets, "blocks": args.blocks,
+                   **({"tp_share": args.tp_share, "I_full": full_I} if args.tp_share > 1 else {}),
                    "routed_experts": round(main_m["routed"], 2), "eligible": round(main_m["sprime"], 2),
                    "natural_union": round(main_m["unat"], 2)},
         "roofline": {"bound": "hbm", "kernel": "acceptmoe_moe_forward (gate_up with per-item dispatch + down with in-LDS combine)",

@@ -1083,12 +1083,14 @@ hipError_t launch_down_rows(const ForwardParams& p, int cap, hipStream_t stream)
 
 // Column-tile down pass shape: I split in two when that keeps the grid near
 // 256 workgroups, two column tiles per workgroup for wide H, k-steps per
-// pipeline stage: the largest of 12, 8, 6, 4, 2, 1 dividing the part of I,
+// pipeline stage: the largest of 12, 8, 6, 4, 3, 2, 1 dividing the part of I,
 // at most 12 with one column tile (two stages in flight then fit the
 // registers of one 8-wave workgroup per CU, and the deeper stages keep more
 // bytes in flight: 12 vs 4 k-steps measured 0.6 us faster at H = 2048,
 // I = 768) and at most 4 with two (whose stages already carry twice the
-// weight bytes; 8 measured slower at H = 4096, I = 1536).
+// weight bytes; 8 measured slower at H = 4096, I = 1536).  Thin parts of I
+// (one GPU's share of a tensor-parallel split) give lengths like 3, where
+// 3-step stages ran 11 % faster than single steps.
 struct ColShape {
   int ksplit, ku, nb;
 };
@@ -1101,7 +1103,7 @@ ColShape col_shape(int H, int I, int is_bf16) {
   c.ksplit = (ntiles / c.nb <= 128 && KC % 2 == 0) ? 2 : 1;
   const int len = KC / c.ksplit;
   c.ku = 1;
-  for (const int u : {12, 8, 6, 4, 2}) {
+  for (const int u : {12, 8, 6, 4, 3, 2}) {
     if (len % u == 0 && u <= (c.nb == 1 ? 12 : 4)) {
       c.ku = u;
       break;
@@ -1130,6 +1132,7 @@ hipError_t launch_down_col_nb(const ForwardParams& p, const ColShape& c, hipStre
     }
   }
   if (c.ku == 4) down_col_kernel<P, 4, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+  else if (c.ku == 3) down_col_kernel<P, 3, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
   else if (c.ku == 2) down_col_kernel<P, 2, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
   else down_col_kernel<P, 1, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
   return hipGetLastError();

@@ -345,6 +345,22 @@ def test_forward_parity_path_limits(gpu, T, k, E, dtype):
     assert err <= FWD_TOL[cfg.dtype], err
 
 
+# one GPU's share of a tensor-parallel split over I: thin I gives the column-tile
+# down pass 3-step stages (one column tile at H = 1024, two at H = 4096)
+@pytest.mark.parametrize("H,I,T,E", [(1024, 96, 32, 64), (4096, 192, 64, 32)])
+def test_forward_parity_thin_shard(gpu, H, I, T, E):
+    cfg = W.LayerConfig("thin", 96 + I, "bf16", T=T, B=1, H=H, E=E, k=8, I=I, depth_max=6,
+                        commit_rule="depth_sibling", hidden_std=1.0)
+    rng = np.random.default_rng(H + I)
+    h32 = rng.standard_normal((T, H)).astype(np.float32)
+    idx = np.stack([rng.permutation(E)[:cfg.k] for _ in range(T)]).astype(np.int32)
+    gate = rng.random((T, cfg.k)).astype(np.float32)
+    say(f"forward thin shard H={H} I={I} T={T} E={E}")
+    got, h64, (wg, wu, wd) = forward_case(cfg, idx, gate, h32)
+    ref = O.moe_forward_grouped(h64, wg, wu, wd, idx, gate, cfg.dtype)
+    assert normwise_rel(got, ref) <= FWD_TOL[cfg.dtype]
+
+
 # fp32 with I / 16 odd: the last gate/up tile pair is half padding (column-tile and per-slot paths)
 @pytest.mark.parametrize("T", [37, 300])
 def test_forward_parity_odd_tile_count(gpu, T):
