@@ -57,7 +57,7 @@ ROUTE_CASES = [("fp32_small", None, None, None), ("qwen3_30b_a3b", None, None, N
                # H % 32 == 16: the last packed chunk is half padding; with these H the
                # hidden state is staged in two blocks, the second holding that one chunk
                ("fp32_small", None, None, 1040), ("qwen3_30b_a3b", 21, 40, 2064),
-               ("fp32_small", None, 24, 48)]
+               ("fp32_small", None, 24, 48), ("qwen3_30b_a3b", 1, None, None)]
 
 
 @pytest.mark.parametrize("name,T,E,H", ROUTE_CASES)
