@@ -356,11 +356,15 @@ __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f +
 #ifndef AMOE_GU_KS
 #define AMOE_GU_KS 4
 #endif
+// per-slot down pass (blocks of more than 256 tokens): four H-tiles per wave
+// share each activation fragment, two waves split I (against two tiles and
+// four waves: 1036 vs 1103 us for the whole forward at T = 512, H = 4096,
+// I = 1536, where the activation reads had outweighed the weight reads)
 #ifndef AMOE_DN_NTW
-#define AMOE_DN_NTW 2
+#define AMOE_DN_NTW 4
 #endif
 #ifndef AMOE_DN_KS
-#define AMOE_DN_KS 4
+#define AMOE_DN_KS 2
 #endif
 
 #ifndef AMOE_NT_WEIGHTS
