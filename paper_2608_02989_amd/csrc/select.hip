@@ -75,29 +75,12 @@ struct NodeScratch {
   NodeSlot s[kNodeWaves];
 };
 
-// Wave minimum of 32- or 64-bit keys, broadcast (the DPP steps of dpp::reduce).
+// Wave minimum of 32-bit keys, broadcast (the DPP steps of dpp::reduce).
 __device__ __forceinline__ uint32_t wave_min_key(uint32_t v) {
   return dpp::reduce(v, 0xffffffffu, [](uint32_t x, uint32_t y) { return min(x, y); });
 }
-template <int Ctrl, int RowMask = 0xf>
-__device__ __forceinline__ uint64_t mov64(uint64_t old, uint64_t v) {
-  const uint32_t lo = dpp::mov<Ctrl, RowMask>(static_cast<uint32_t>(old), static_cast<uint32_t>(v));
-  const uint32_t hi = dpp::mov<Ctrl, RowMask>(static_cast<uint32_t>(old >> 32), static_cast<uint32_t>(v >> 32));
-  return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-__device__ __forceinline__ uint64_t wave_min_key(uint64_t v) {
-  const uint64_t id = ~0ull;
-  v = min(v, mov64<dpp::kXor1>(id, v));
-  v = min(v, mov64<dpp::kXor2>(id, v));
-  v = min(v, mov64<dpp::kHalfMirror>(id, v));
-  v = min(v, mov64<dpp::kMirror>(id, v));
-  v = min(v, mov64<dpp::kBcast15, 0xA>(id, v));
-  v = min(v, mov64<dpp::kBcast31, 0xC>(id, v));
-  return (static_cast<uint64_t>(dpp::lane63(static_cast<uint32_t>(v >> 32))) << 32) |
-         dpp::lane63(static_cast<uint32_t>(v));
-}
 
-// k-th largest key among the wave's EPL*64 keys (32- or 64-bit), for NN
+// k-th largest key among the wave's EPL*64 32-bit keys, for NN
 // nodes at once (0 if fewer than k keys are non-zero).  The key is built from
 // the top bit down: cand grows while at least k keys stay >= cand.  Once
 // exactly k keys are >= cand that count stays k, those keys are the top k and
@@ -203,33 +186,43 @@ __device__ __forceinline__ int slot_of(int j, int n, const uint32_t* sk, const i
 // share the slice, so their LDS reads are broadcasts); the partial counts are
 // stored and added per expert after a barrier.  The caller synchronizes
 // before reading rank.
+// slices of the index range per expert in rank_item (E * parts <= kSelThreads)
+__device__ __forceinline__ int rank_parts(int E) { return E <= 128 ? 8 : (E <= 256 ? 4 : 2); }
+
+// Partial rank of flagged expert e (item = part * E + e): the flagged
+// competitors in index slice `part` that come before e in (v desc or asc,
+// index asc) order; 0 for an unflagged e.  Eight broadcast values per LDS
+// step (flags past E are 0, reads stay inside the kMaxExperts arrays).
+template <bool kDesc>
+__device__ __forceinline__ int rank_item(const double* v, const uint8_t* flag, int E, int parts, int item) {
+  const int span = ((E + parts - 1) / parts + 7) & ~7;  // competitors per slice, multiple of 8
+  const int part = item / E, e = item % E;
+  const double ve = v[e];
+  const int j_begin = part * span;
+  const int j_end = min(E, j_begin + span);
+  int r = 0;
+  for (int j0 = j_begin; j0 < j_end; j0 += 8) {
+    const double2 a = *reinterpret_cast<const double2*>(v + j0);
+    const double2 b = *reinterpret_cast<const double2*>(v + j0 + 2);
+    const double2 c = *reinterpret_cast<const double2*>(v + j0 + 4);
+    const double2 d = *reinterpret_cast<const double2*>(v + j0 + 6);
+    const uint2 f = *reinterpret_cast<const uint2*>(flag + j0);
+    const double vv[8] = {a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const bool fl = ((q < 4 ? f.x >> (8 * q) : f.y >> (8 * (q - 4))) & 0xffu) != 0u;
+      const bool beats = kDesc ? (vv[q] > ve) : (vv[q] < ve);
+      r += static_cast<int>(fl & (beats | ((vv[q] == ve) & (j0 + q < e))));
+    }
+  }
+  return flag[e] ? r : 0;
+}
+
 template <bool kDesc>
 __device__ __forceinline__ void rank_all(const double* v, const uint8_t* flag, int E, int* rank, int* part_cnt,
                                          int tid) {
-  const int parts = E <= 128 ? 8 : (E <= 256 ? 4 : 2);
-  const int span = ((E + parts - 1) / parts + 7) & ~7;  // competitors per slice, multiple of 8
-  for (int item = tid; item < E * parts; item += kSelThreads) {
-    const int part = item / E, e = item % E;
-    const double ve = v[e];
-    const int j_begin = part * span;
-    const int j_end = min(E, j_begin + span);
-    int r = 0;
-    for (int j0 = j_begin; j0 < j_end; j0 += 8) {
-      const double2 a = *reinterpret_cast<const double2*>(v + j0);
-      const double2 b = *reinterpret_cast<const double2*>(v + j0 + 2);
-      const double2 c = *reinterpret_cast<const double2*>(v + j0 + 4);
-      const double2 d = *reinterpret_cast<const double2*>(v + j0 + 6);
-      const uint2 f = *reinterpret_cast<const uint2*>(flag + j0);
-      const double vv[8] = {a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const bool fl = ((q < 4 ? f.x >> (8 * q) : f.y >> (8 * (q - 4))) & 0xffu) != 0u;
-        const bool beats = kDesc ? (vv[q] > ve) : (vv[q] < ve);
-        r += static_cast<int>(fl & (beats | ((vv[q] == ve) & (j0 + q < e))));
-      }
-    }
-    part_cnt[item] = flag[e] ? r : 0;
-  }
+  const int parts = rank_parts(E);
+  for (int item = tid; item < E * parts; item += kSelThreads) part_cnt[item] = rank_item<kDesc>(v, flag, E, parts, item);
   __syncthreads();
   if (tid < E) {
     int r = 0;
@@ -396,31 +389,29 @@ __device__ __forceinline__ int count_before(const double* v, int n, double vj, i
 
 // ---------------------------------------------------------------------------
 // Eq. 6, Sec. 3.3 and Eq. 7 for the self-sizing and fixed-budget modes, run
-// by one wave (lane l holds experts l, l + 64, ...) without workgroup
-// barriers.  Sums take the same per-lane order and wave reduction as the
-// workgroup path, integer counts are order-free, so the results are the same.
-// Writes inS, inSp, rankv (pruning order, -1 outside C), pv and the scalars.
+// by one wave (lane l holds experts l, l + 64, ...) in two parts around one
+// workgroup barrier: eligible_take_wave finds n_er and the number of R
+// members S takes while the other waves rank the positive members of R
+// (rank_item over sh.inC); eligible_set_wave then builds S from those ranks,
+// |S|, a(S) and the Eq. 7 pruning.  Sums take the same per-lane order and
+// wave reduction as the workgroup path, integer counts are order-free, so the
+// results are the same.
 // ---------------------------------------------------------------------------
 template <int EPL>
-__device__ void eligible_set_wave(SelShared& sh, int mode, int E, int k, int bud, int removal_cap, bool prune,
-                                  int lane) {
+__device__ void eligible_take_wave(SelShared& sh, int mode, int E, int k, int bud, int lane) {
   const int kmin = min(k, E);
-  double u[EPL];
-  bool ok[EPL], inR[EPL], inS[EPL];
-#pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    const int e = lane + kWave * i;
-    ok[i] = e < E;
-    u[i] = ok[i] ? sh.u[e] : 0.0;
-    inR[i] = ok[i] && sh.inR[e];
-    if (ok[i]) {
-      sh.inS[e] = sh.anchor[e];
-      sh.rankv[e] = -1;
-    }
-  }
   const int n_anchor = sh.n_anchor, n_R = sh.n_R, n_pos = sh.n_pos;
   int ner, take;
   if (mode == MODE_SELF) {
+    double u[EPL];
+    bool ok[EPL], inR[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = lane + kWave * i;
+      ok[i] = e < E;
+      u[i] = ok[i] ? sh.u[e] : 0.0;
+      inR[i] = ok[i] && sh.inR[e];
+    }
     // Z = sum over R of u^+ ; H = -sum q log q ; n_er = ceil(exp(H) - 1e-9)   (Eq. 6)
     double zp = 0.0;
 #pragma unroll
@@ -456,33 +447,44 @@ __device__ void eligible_set_wave(SelShared& sh, int mode, int E, int k, int bud
     if (take > n_R) take = n_R;
     ner = take;
   }
+  if (lane == 0) {
+    sh.n_er = ner;
+    sh.n_take = take;
+  }
+}
+
+// Writes inS, inSp, rankv (pruning order, -1 outside C), pv and the scalars
+// |S|, a(S), |C|, m*.  part_cnt: the `parts` partial ranks of every positive
+// member of R (rank_item over sh.inC).
+template <int EPL>
+__device__ void eligible_set_wave(SelShared& sh, int E, int k, int parts, const int* part_cnt, int removal_cap,
+                                  bool prune, int lane) {
+  const int take = sh.n_take;
+  double u[EPL];
+  bool ok[EPL], inR[EPL], inS[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + kWave * i;
+    ok[i] = e < E;
+    u[i] = ok[i] ? sh.u[e] : 0.0;
+    inR[i] = ok[i] && sh.inR[e];
+    if (ok[i]) {
+      sh.inS[e] = sh.anchor[e];
+      sh.rankv[e] = -1;
+    }
+  }
   // S = A u first `take` of R in (u desc, index asc) order: members with u > 0
-  // by a top-`take` search over their utilities' bit patterns (u > 0, so the
-  // bits order like the values; equal utilities go lowest index first), then
-  // u = 0 members in index order if needed
-  uint64_t ukey[1][EPL];
+  // by their rank among themselves, then u = 0 members in index order if needed
   int np = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const bool f = inR[i] && u[i] > 0.0;
-    ukey[0][i] = f ? static_cast<uint64_t>(__double_as_longlong(u[i])) : 0ull;
     np += popc64(__ballot(f));
-  }
-  if (take > 0 && np > 0) {
-    uint64_t thr[1];
-    kth_largest<EPL, 1>(ukey, take, thr);
-    int greater = 0;
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) greater += popc64(__ballot(ukey[0][i] > thr[0]));
-    const int need = take - greater;
-    const uint64_t below = lanes_below(lane);
-    int eq_before = 0;
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      const bool eq = ukey[0][i] == thr[0] && ukey[0][i] != 0ull;
-      const uint64_t eqm = __ballot(eq);
-      if ((ukey[0][i] > thr[0]) | (eq & ((eq_before + popc64(eqm & below)) < need))) sh.inS[lane + kWave * i] = 1;
-      eq_before += popc64(eqm);
+    if (f) {
+      const int e = lane + kWave * i;
+      int r = 0;
+      for (int q = 0; q < parts; ++q) r += part_cnt[q * E + e];
+      if (r < take) sh.inS[e] = 1;
     }
   }
   if (take > np) {
@@ -558,8 +560,6 @@ __device__ void eligible_set_wave(SelShared& sh, int mode, int E, int k, int bud
     }
   }
   if (lane == 0) {
-    sh.n_er = ner;
-    sh.n_take = take;
     sh.n_S = nS;
     sh.budget_a = aS;
     sh.n_C = nC;
@@ -676,6 +676,7 @@ __device__ __forceinline__ void tree_p3(SelShared& sh, const SelectParams& p, co
   if (in_e) {
     sh.u[tid] = u_acc;
     sh.inR[tid] = !anc;
+    sh.inC[tid] = !anc && u_acc > 0.0;  // positive member of R (ranked in P4; every mode resets inC there)
   }
   wg_count(anc, &sh.n_anchor, lane);
   wg_count(in_e && sh.votes[tid] > 0, &sh.n_unat, lane);
@@ -693,8 +694,17 @@ __device__ __forceinline__ void tree_p4(SelShared& sh, const SelectParams& p, co
   const int bud = p.budget < kmin ? kmin : (p.budget > E ? E : p.budget);
 
   if (mode == MODE_SELF || mode == MODE_FIXED) {
-    // Eq. 6, S, |S|, a(S) and the Eq. 7 pruning in one wave
-    if (wave == 0) eligible_set_wave<EPL>(sh, mode, E, k, bud, p.removal_cap, p.resident != nullptr, lane);
+    // Eq. 6 in wave 0 while the other waves rank the positive members of R;
+    // then S, |S|, a(S) and the Eq. 7 pruning in wave 0
+    const int parts = rank_parts(E);
+    if (wave == 0) {
+      eligible_take_wave<EPL>(sh, mode, E, k, bud, lane);
+    } else {
+      for (int item = tid - kWave; item < E * parts; item += kSelThreads - kWave)
+        sh.rpart[item] = rank_item<true>(sh.u, sh.inC, E, parts, item);
+    }
+    __syncthreads();
+    if (wave == 0) eligible_set_wave<EPL>(sh, E, k, parts, sh.rpart, p.removal_cap, p.resident != nullptr, lane);
     __syncthreads();
   } else {
     if (mode == MODE_MOESPEC || mode == MODE_COUNT) {
