@@ -234,6 +234,35 @@ def test_select_parity_batch_with_invalid_trees(gpu, sizes):
     assert_select_equal(got, ref, "batch with invalid trees")
 
 
+# the largest batch of trees: ACCEPTMOE_MAX_TREES ragged trees (empty ones
+# included), with a residency mask and in the fixed-budget mode
+@pytest.mark.parametrize("mode,budget", [(L.MODE_SELF_SIZING, 0), (L.MODE_FIXED_BUDGET, 12)])
+def test_select_parity_max_trees(gpu, mode, budget):
+    rng = np.random.default_rng(21)
+    E, k = 64, 4
+    sizes = rng.integers(0, 10, size=L.MAX_TREES)
+    sizes[0], sizes[-1] = 0, 9
+    pars, deps, probs = [], [], []
+    offs = [0]
+    for s_ in sizes:
+        s_ = int(s_)
+        par, dep, sib = W.make_tree(rng, s_, 4) if s_ else (np.zeros(0, np.int32),) * 3
+        pars.append(np.where(par < 0, -1, par + offs[-1]))
+        deps.append(dep)
+        probs.append((0.75 ** dep * 0.6 ** sib).astype(np.float32))
+        offs.append(offs[-1] + s_)
+    par = np.concatenate(pars).astype(np.int32)
+    dep = np.concatenate(deps).astype(np.int32)
+    prob = np.concatenate(probs).astype(np.float32)
+    z32 = rng.standard_normal((offs[-1], E)).astype(np.float32)
+    resident = (rng.random(E) < 0.3).astype(np.uint8)
+    say(f"select {L.MAX_TREES} trees T={offs[-1]} mode={mode}")
+    got, ref = run_select_both(z32, par, dep, prob, offs, k, mode=mode, budget=budget, resident=resident)
+    codes = got["stats"][:, L.NUM_STATS - 2]
+    assert (codes[sizes == 0] == O.TREE_EMPTY).all() and (codes[sizes > 0] == 0).all()
+    assert_select_equal(got, ref, f"{L.MAX_TREES} trees")
+
+
 # ---------------------------------------------------------------------------
 # forward
 # ---------------------------------------------------------------------------
