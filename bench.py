@@ -116,8 +116,8 @@ def main():
         estimate_report(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this layer runs on a single MI355X "
-              "(multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
+        print("bench.py measures one GPU only: the layer runs on a single MI355X; "
+              "sharding it over several GPUs is designed but not built", file=sys.stderr)
         sys.exit(2)
 
     import torch
