@@ -60,7 +60,7 @@ struct SelShared {
   alignas(16) uint8_t routed[kMaxExperts];
   alignas(16) uint8_t resident[kMaxExperts];
   alignas(16) int rpart[kSelThreads];  // partial rank counts
-  alignas(16) int plist[kMaxExperts];     // compacted expert lists (index order) ...
+  alignas(16) int plist[kMaxExperts];     // compacted expert lists (positive R members, then C) ...
   alignas(16) double pval[kMaxExperts];   // ... and their utilities
 };
 
@@ -231,6 +231,28 @@ __device__ __forceinline__ void rank_all(const double* v, const uint8_t* flag, i
   }
 }
 
+// Rank counts of the n compacted values pval[i] (expert plist[i]) in (value
+// desc, expert asc) order: item = (slice q, entry i) counts the entries of
+// slice q that come before entry i and adds that into cnt[i] (integer LDS
+// atomics, so the order of the adds does not matter).
+__device__ __forceinline__ void rank_compact(const double* pval, const int* plist, int n, int* cnt, int first,
+                                             int stride) {
+  const int parts = max(1, (n + 15) / 16);
+  const int span = (n + parts - 1) / parts;
+  for (int item = first; item < n * parts; item += stride) {
+    const int q = item / n, i = item % n;
+    const double vi = pval[i];
+    const int ei = plist[i];
+    const int j_end = min(n, (q + 1) * span);
+    int r = 0;
+    for (int j = q * span; j < j_end; ++j) {
+      const double vj = pval[j];
+      r += static_cast<int>((vj > vi) | ((vj == vi) & (plist[j] < ei)));
+    }
+    if (r) atomicAdd(&cnt[i], r);
+  }
+}
+
 // Workgroup counters without contention: each wave adds its ballot count (or
 // its lane sum) with a single LDS atomic.  Integer sums, so the order of the
 // atomics does not change the result.
@@ -392,7 +414,8 @@ __device__ __forceinline__ int count_before(const double* v, int n, double vj, i
 // by one wave (lane l holds experts l, l + 64, ...) in two parts around one
 // workgroup barrier: eligible_take_wave finds n_er and the number of R
 // members S takes while the other waves rank the positive members of R
-// (rank_item over sh.inC); eligible_set_wave then builds S from those ranks,
+// (rank_compact over the list P3 compacts); eligible_set_wave then builds S
+// from those ranks,
 // |S|, a(S) and the Eq. 7 pruning.  Sums take the same per-lane order and
 // wave reduction as the workgroup path, integer counts are order-free, so the
 // results are the same.
@@ -454,11 +477,10 @@ __device__ void eligible_take_wave(SelShared& sh, int mode, int E, int k, int bu
 }
 
 // Writes inS, inSp, rankv (pruning order, -1 outside C), pv and the scalars
-// |S|, a(S), |C|, m*.  part_cnt: the `parts` partial ranks of every positive
-// member of R (rank_item over sh.inC).
+// |S|, a(S), |C|, m*.  On entry plist / pval hold the positive members of R
+// and pv their ranks (rank_compact).
 template <int EPL>
-__device__ void eligible_set_wave(SelShared& sh, int E, int k, int parts, const int* part_cnt, int removal_cap,
-                                  bool prune, int lane) {
+__device__ void eligible_set_wave(SelShared& sh, int E, int k, int removal_cap, bool prune, int lane) {
   const int take = sh.n_take;
   double u[EPL];
   bool ok[EPL], inR[EPL], inS[EPL];
@@ -475,18 +497,10 @@ __device__ void eligible_set_wave(SelShared& sh, int E, int k, int parts, const 
   }
   // S = A u first `take` of R in (u desc, index asc) order: members with u > 0
   // by their rank among themselves, then u = 0 members in index order if needed
-  int np = 0;
-#pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    const bool f = inR[i] && u[i] > 0.0;
-    np += popc64(__ballot(f));
-    if (f) {
-      const int e = lane + kWave * i;
-      int r = 0;
-      for (int q = 0; q < parts; ++q) r += part_cnt[q * E + e];
-      if (r < take) sh.inS[e] = 1;
-    }
-  }
+  const int np = sh.n_pos;
+  wave_lds_sync();  // inS reset above before the members are set
+  for (int i = lane; i < np; i += kWave)
+    if (sh.pv[i] < take) sh.inS[sh.plist[i]] = 1;
   if (take > np) {
     int base = 0;
 #pragma unroll
@@ -676,12 +690,24 @@ __device__ __forceinline__ void tree_p3(SelShared& sh, const SelectParams& p, co
   if (in_e) {
     sh.u[tid] = u_acc;
     sh.inR[tid] = !anc;
-    sh.inC[tid] = !anc && u_acc > 0.0;  // positive member of R (ranked in P4; every mode resets inC there)
   }
   wg_count(anc, &sh.n_anchor, lane);
   wg_count(in_e && sh.votes[tid] > 0, &sh.n_unat, lane);
   wg_count(in_e && !anc, &sh.n_R, lane);
-  wg_count(in_e && !anc && u_acc > 0.0, &sh.n_pos, lane);
+  // the positive members of R, compacted (in no particular order) into
+  // plist / pval for the ranking of P4, with their rank counters pv zeroed;
+  // n_pos is their number
+  const bool pos = in_e && !anc && u_acc > 0.0;
+  const uint64_t pm = __ballot(pos);
+  int pbase = 0;
+  if (lane == 0 && pm != 0ull) pbase = atomicAdd(&sh.n_pos, popc64(pm));
+  pbase = __builtin_amdgcn_readfirstlane(pbase);
+  if (pos) {
+    const int i = pbase + popc64(pm & lanes_below(lane));
+    sh.plist[i] = tid;
+    sh.pval[i] = u_acc;
+    sh.pv[i] = 0;
+  }
 }
 
 // P4 and the tree's outputs: S' into sh.inSp and eligible[b], statistics
@@ -696,15 +722,12 @@ __device__ __forceinline__ void tree_p4(SelShared& sh, const SelectParams& p, co
   if (mode == MODE_SELF || mode == MODE_FIXED) {
     // Eq. 6 in wave 0 while the other waves rank the positive members of R;
     // then S, |S|, a(S) and the Eq. 7 pruning in wave 0
-    const int parts = rank_parts(E);
-    if (wave == 0) {
+    if (wave == 0)
       eligible_take_wave<EPL>(sh, mode, E, k, bud, lane);
-    } else {
-      for (int item = tid - kWave; item < E * parts; item += kSelThreads - kWave)
-        sh.rpart[item] = rank_item<true>(sh.u, sh.inC, E, parts, item);
-    }
+    else
+      rank_compact(sh.pval, sh.plist, sh.n_pos, sh.pv, tid - kWave, kSelThreads - kWave);
     __syncthreads();
-    if (wave == 0) eligible_set_wave<EPL>(sh, E, k, parts, sh.rpart, p.removal_cap, p.resident != nullptr, lane);
+    if (wave == 0) eligible_set_wave<EPL>(sh, E, k, p.removal_cap, p.resident != nullptr, lane);
     __syncthreads();
   } else {
     if (mode == MODE_MOESPEC || mode == MODE_COUNT) {
