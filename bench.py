@@ -200,13 +200,15 @@ def main():
     def measure(rho, steps, warmup):
         blocks = make_blocks(rho)
         stream = torch.cuda.Stream()
-        # untimed pre-pass: the routed union of every (set, block) pair (selection is deterministic)
-        routed, sprime, unat = {}, {}, {}
+        # untimed pre-pass: the routed union of every (set, block) pair (selection is
+        # deterministic) and its routing, kept for the forward-only timing below
+        routed, sprime, unat, routing = {}, {}, {}, {}
         with torch.cuda.stream(stream):
             for s in range(n_sets):
                 for b in range(args.blocks):
                     _, sel, _ = run_once(blocks, s, b, stream)
                     idx = sel["idx"]
+                    routing[(s, b)] = (idx.clone(), sel["gate"].clone())
                     routed[(s, b)] = int(torch.unique(idx[idx >= 0]).numel())
                     st = sel["stats"].cpu().numpy()
                     sprime[(s, b)] = float(st[:, 4].mean())
@@ -258,15 +260,49 @@ def main():
             torch.cuda.synchronize()
             graph_ms = gs.elapsed_time(ge) / (reps * period) * steps
             del g
+        # (3) the forward launches alone, replayed from a HIP graph over the same
+        # rotation (every (set, block) pair's routing from the pre-pass): the
+        # average launch duration without the host launch cost that the eager
+        # events around each launch include
+        fwd_graph_us, fwd_graph_bytes = None, None
+        if args.graph:
+            pairs = combos(period)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(stream):
+                with torch.cuda.graph(g, stream=stream):
+                    for (s, b) in pairs:
+                        L_, B_ = layers[s], blocks[b]
+                        T = B_["h"].shape[0]
+                        ops.moe_forward(B_["h"], L_.wgu, L_.wd, routing[(s, b)][0], routing[(s, b)][1],
+                                        out=L_.out[:T], workspace=L_.fwd_ws, stream=stream)
+            torch.cuda.synchronize()
+            reps = max(1, (steps + period - 1) // period)
+            for _ in range(2):
+                g.replay()
+            torch.cuda.synchronize()
+            gs, ge = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            gs.record(stream)
+            with torch.cuda.stream(stream):
+                for _ in range(reps):
+                    g.replay()
+            ge.record(stream)
+            torch.cuda.synchronize()
+            fwd_graph_us = gs.elapsed_time(ge) * 1e3 / (reps * period)
+            fwd_graph_bytes = float(np.mean([routed[c] * ebytes for c in pairs])) + act_bytes
+            del g
         total_ms = graph_ms if graph_ms is not None else eager_ms
         return dict(
             ms_per_step=total_ms / steps,
             eager_us=eager_ms / steps * 1e3,
             graph_us=None if graph_ms is None else graph_ms / steps * 1e3,
             value=float(weight_bytes.sum() / (total_ms * 1e-3) / 1e9),
-            fwd_us=float(np.mean(fwd_ms) * 1e3),
-            fwd_gbs=float(fwd_bytes.sum() / (np.sum(fwd_ms) * 1e-3) / 1e9),
-            fwd_bytes_per_launch=float(fwd_bytes.mean()),
+            fwd_us=float(np.mean(fwd_ms) * 1e3) if fwd_graph_us is None else fwd_graph_us,
+            fwd_gbs=(float(fwd_bytes.sum() / (np.sum(fwd_ms) * 1e-3) / 1e9) if fwd_graph_us is None
+                     else fwd_graph_bytes / (fwd_graph_us * 1e-6) / 1e9),
+            fwd_bytes_per_launch=float(fwd_bytes.mean()) if fwd_graph_bytes is None else fwd_graph_bytes,
+            fwd_eager_us=float(np.mean(fwd_ms) * 1e3),
+            fwd_eager_gbs=float(fwd_bytes.sum() / (np.sum(fwd_ms) * 1e-3) / 1e9),
+            fwd_timing="HIP graph of forward launches" if fwd_graph_us is not None else "eager HIP events",
             routed=float(r.mean()), sprime=float(np.mean([sprime[c] for c in timed])),
             unat=float(np.mean([unat[c] for c in timed])),
             flops=float(Ttot * cfg.k * 6 * cfg.H * cfg.I + 2 * Ttot * cfg.E * cfg.H),
@@ -325,6 +361,9 @@ def main():
                                  else round(measured_traffic() * main_m["fwd_bytes_per_launch"])),
                      "bytes_per_launch": round(main_m["fwd_bytes_per_launch"]),
                      "launch_us": round(main_m["fwd_us"], 2),
+                     "launch_timing": main_m["fwd_timing"],
+                     "eager_launch_us": round(main_m["fwd_eager_us"], 2),
+                     "eager_achieved": round(main_m["fwd_eager_gbs"], 1),
                      "mfma_util": round(main_m["flops"] / (main_m["fwd_us"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5)},
         "cpu_baseline": cpu,
         "alt_iid": alt,
