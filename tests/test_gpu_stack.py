@@ -114,3 +114,53 @@ def test_stack_graph_replay_and_two_streams(gpu):
         o2 = twin.step(inputs[1][0], *inputs[1][1], stream=s2)
     torch.cuda.synchronize()
     assert np.array_equal(bits(o1), eager[0]) and np.array_equal(bits(o2), eager[1])
+
+
+def test_stack_full_size_48_layers(gpu):
+    """The 48-layer Qwen3-30B-A3B-shaped stack at its full size (T = 60 nodes,
+    the pass bench.py times), teacher-forced per layer: logits, routing, gates
+    and the residual add on every layer; the full expert output on four
+    sampled layers (their weights regenerated from the same seeds)."""
+    cfg = W.CONFIGS["qwen3_30b_a3b_x48"]
+    T = cfg.T
+    layers = []
+    for l in range(cfg.layers):
+        wg, wu, wd = W.expert_weights_torch(cfg, l, DEV)
+        layers.append(ops.VerifyLayer(torch.from_numpy(W.router_weights(cfg, l)).to(DEV), wg, wu, wd, cfg.k,
+                                      max_tokens=T))
+        del wg, wu, wd
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    stack = ops.VerifyStack(layers, T)
+    blk = W.make_block(cfg, block=5, layer=0, rho=0.9, tree_layer=0)
+    h0 = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(DEV)
+    tree = tuple(torch.from_numpy(a).to(DEV) for a in (blk.parent, blk.depth, blk.prob))
+    say(f"full-size stack: {cfg.layers} layers, T={T}")
+    stack.step(h0, *tree)
+    torch.cuda.synchronize()
+    sampled = {0, 16, 33, cfg.layers - 1}
+    sizes = []
+    for l, layer in enumerate(stack.layers):
+        hb = bits(stack.h[l][:T]).view(np.uint16)
+        h64 = O.widen_bf16(hb)
+        z_gpu = layer.logits[:T].cpu().numpy()
+        rw = W.router_weights(cfg, l)
+        assert normwise_rel(z_gpu, O.route(h64, rw.astype(np.float64))) <= LOGIT_TOL, l
+        ref = O.select(z_gpu, blk.parent, blk.depth, blk.prob, None, cfg.k)
+        assert not ref["ambiguous"].any(), l
+        assert np.array_equal(layer.sel_out["idx"][:T].cpu().numpy(), ref["idx"]), l
+        assert np.array_equal(layer.sel_out["eligible"][:1].cpu().numpy(), ref["eligible"]), l
+        assert np.allclose(layer.sel_out["gate"][:T].cpu().numpy(), ref["gate"], rtol=GATE_RTOL, atol=0), l
+        sizes.append(int(ref["eligible"].sum()))
+        y = layer.out[:T].cpu().numpy()
+        if l in sampled:
+            wg, wu, wd = W.expert_weights_torch(cfg, l, DEV)
+            y_ref = O.moe_forward_grouped(h64, HostExperts(wg), HostExperts(wu), HostExperts(wd), ref["idx"],
+                                          ref["gate"], "bf16")
+            del wg, wu, wd
+            err = normwise_rel(y, y_ref)
+            say(f"  layer {l}: |S'| = {sizes[-1]}, output error {err:.2e}")
+            assert err <= FWD_TOL["bf16"], (l, err)
+        want = W.bf16_round(h64.astype(np.float32) + y)
+        assert np.array_equal(bits(stack.h[l + 1][:T]).view(np.uint16), want), l
+    say(f"  |S'| over the layers: min {min(sizes)}, mean {np.mean(sizes):.1f}, max {max(sizes)}")
