@@ -6,11 +6,16 @@ inputs resident in HBM.  Steps rotate over several independently seeded
 layers (weight sets) and blocks so consecutive steps never reuse expert
 weights through the 256 MB Infinity Cache.
 
-Prints one JSON line:
+The headline workload is the largest single-tree configuration (H = 4096,
+I = 1536, T = 64 nodes, 25 % residency mask); the Qwen3-30B-A3B-shaped layer
+(T = 32) and the batched one (8 trees x 64 nodes) follow as companions, each
+with its own roofline block.  Prints one JSON line:
   value      eligible-expert weight bytes streamed per second (GB/s) over the
-             whole step (route + select + forward)
+             whole step (route + select + forward), bytes and time over the
+             same timed steps
   roofline   the expert FFN launch (acceptmoe_moe_forward) against HBM peak,
-             its duration measured with HIP events around every timed launch
+             timed with HIP events around graph replays of the timed steps'
+             forward launches; traffic from committed rocprofv3 counters
   cpu_baseline  the CPU oracle on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -31,16 +36,26 @@ HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 
 
+DEFAULT_CONFIG = "wide_offload"
+COMPANIONS = "qwen3_30b_a3b,batched_8x64"
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=40)
-    ap.add_argument("--config", default="qwen3_30b_a3b")
+    ap.add_argument("--config", default=DEFAULT_CONFIG,
+                    help="headline workload (default: H=4096, I=1536, T=64 with a 25%% residency mask, the largest "
+                         "single-tree configuration)")
+    ap.add_argument("--companions", default=COMPANIONS,
+                    help="comma-separated workloads timed after the headline, each with its own roofline "
+                         "block ('' = none)")
     ap.add_argument("--rho", type=float, default=0.9, help="tree correlation of hidden states")
     ap.add_argument("--sets", type=int, default=0, help="weight sets to rotate (0 = enough for >= 2 GiB)")
     ap.add_argument("--blocks", type=int, default=16)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle sample budget (0 = skip)")
+    ap.add_argument("--cpu-seconds-1t", type=float, default=8.0, help="single-thread oracle sample budget")
     ap.add_argument("--no-alt", action="store_true", help="skip the i.i.d. (rho = 0) companion run")
     ap.add_argument("--graph", type=int, default=1, help="time HIP-graph replays of the step sequence (1/0)")
     ap.add_argument("--stack-blocks", type=int, default=8, help="blocks timed through a whole layer stack")
@@ -53,6 +68,9 @@ def parse():
     ap.add_argument("--phys-layers", type=int, default=4, help="layers of the physical (copying) offload run")
     ap.add_argument("--estimate", action="store_true",
                     help="offline commitment estimator report (p_hat from synthetic traces, tree and chain blocks)")
+    ap.add_argument("--modes", action="store_true",
+                    help="selector modes at a matched budget B_0 (AcceptMoE, AcceptMoE-B, MoE-Spec, Count-B, "
+                         "natural routing): set sizes, routed experts and bytes, step latency")
     ap.add_argument("--tp-share", type=int, default=1, metavar="G",
                     help="time one GPU's share of a G-way tensor-parallel split over I: the same routing "
                          "(router, hidden states and trees as the full layer), experts with I/G rows")
@@ -61,7 +79,11 @@ def parse():
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "moe_forward_qwen3_30b_a3b_traffic.md")
+# Measured HBM traffic of the forward per workload: one line per configuration,
+# "traffic: config=NAME source_hash=H ratio=R ...", R = counted bytes /
+# algorithmic bytes of one launch; a line applies only while the forward
+# sources still hash to H.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "moe_forward_traffic.md")
 FFN_SOURCES = ["paper_2608_02989_amd/csrc/forward.hip", "paper_2608_02989_amd/csrc/common.hpp"]
 
 
@@ -74,23 +96,23 @@ def ffn_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """Measured / algorithmic HBM bytes of a forward launch from the committed
-    counter summary, or None when it is missing or the kernels changed since."""
+def measured_traffic(config: str):
+    """Measured / algorithmic HBM bytes of a forward launch of `config` from the
+    committed counter summary; None when that configuration was not measured
+    or the kernels changed since."""
     try:
         with open(TRAFFIC_FILE) as f:
             text = f.read()
     except OSError:
         return None
-    vals = {}
+    want = ffn_source_hash()
     for line in text.splitlines():
-        if line.startswith("traffic:"):
-            for kv in line[len("traffic:"):].split():
-                k, _, v = kv.partition("=")
-                vals[k] = v
-    if vals.get("source_hash") != ffn_source_hash() or "ratio" not in vals:
-        return None
-    return float(vals["ratio"])
+        if not line.startswith("traffic:"):
+            continue
+        vals = dict(kv.partition("=")[::2] for kv in line[len("traffic:"):].split())
+        if vals.get("config") == config and vals.get("source_hash") == want and "ratio" in vals:
+            return float(vals["ratio"])
+    return None
 
 
 def copy_calibration(mb: int) -> None:
@@ -102,6 +124,251 @@ def copy_calibration(mb: int) -> None:
         dst.copy_(src)
     torch.cuda.synchronize()
     print(f"copied {mb} MiB five times", flush=True)
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def _pct(x, q):
+    return round(float(np.percentile(np.asarray(x, np.float64), q)), 2)
+
+
+class Workload:
+    """One configuration's resident weight sets (VerifyLayer each) and seeded blocks."""
+
+    def __init__(self, name, args, log, tp_share=1, sets=0):
+        import torch
+
+        from paper_2608_02989_amd import ops
+        from paper_2608_02989_amd import workload as W
+
+        self.dev = "cuda"
+        cfg = W.CONFIGS[name]
+        self.full_I = cfg.I
+        if tp_share > 1:
+            # one GPU's shard: the seeds depend on the configuration id, not on I,
+            # so routing is the full layer's and only the expert weights shrink
+            if cfg.I % (32 * tp_share) != 0:
+                raise SystemExit(f"--tp-share {tp_share}: I = {cfg.I} does not split into multiples of 32")
+            cfg = W.LayerConfig(**{**cfg.__dict__, "I": cfg.I // tp_share})
+        self.cfg, self.tp_share, self.nblocks = cfg, tp_share, args.blocks
+        self.T = cfg.total_tokens
+        self.ebytes = cfg.expert_bytes
+        layer_bytes = cfg.E * self.ebytes
+        # enough independently seeded layers that consecutive steps never reuse
+        # weights through the 256 MB Infinity Cache
+        n = sets or max(2 if cfg.B > 1 else 4, int(np.ceil(2 * 2**30 / layer_bytes)))
+        self.n_sets = min(n, 16)
+        log(f"config {cfg.name} T={self.T} B={cfg.B} H={cfg.H} E={cfg.E} k={cfg.k} I={cfg.I} "
+            f"dtype={cfg.dtype} sets={self.n_sets} blocks={self.nblocks}")
+        self.layers = []
+        for s in range(self.n_sets):
+            rw = torch.from_numpy(W.router_weights(cfg, s)).to(self.dev)
+            wg, wu, wd = W.expert_weights_torch(cfg, s, self.dev)
+            self.layers.append(ops.VerifyLayer(rw, wg, wu, wd, cfg.k, max_tokens=self.T, max_trees=cfg.B))
+            del wg, wu, wd
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        log("weights generated and packed")
+
+    def blocks(self, rho):
+        import torch
+
+        from paper_2608_02989_amd import workload as W
+        out = []
+        for b in range(self.nblocks):
+            blk = W.make_block(self.cfg, block=b, layer=0, rho=rho)
+            if self.cfg.dtype == "bf16":
+                h = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(self.dev)
+            else:
+                h = torch.from_numpy(blk.hidden).to(self.dev)
+            out.append(dict(
+                h=h, parent=torch.from_numpy(blk.parent).to(self.dev),
+                depth=torch.from_numpy(blk.depth).to(self.dev), prob=torch.from_numpy(blk.prob).to(self.dev),
+                offs=blk.offsets.tolist(),
+                resident=None if blk.resident is None else torch.from_numpy(blk.resident).to(self.dev), host=blk))
+        return out
+
+    def free(self):
+        import torch
+        self.layers = []
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
+def measure(wl: Workload, rho, steps, warmup, graph=True, min_graph_steps=100):
+    """Times `steps` steps (after `warmup` untimed ones) of one workload.
+
+    A step is route -> select -> forward of one block through one weight set;
+    steps rotate over (weight set, block) pairs.  The same timed sequence is
+    (1) launched eagerly with HIP events around every step and every forward,
+    (2) captured in one HIP graph and replayed (the headline time), and (3)
+    its forward launches alone, with the routing of an untimed pre-pass, in a
+    second graph (the forward's roofline).  Bytes are summed over exactly the
+    timed steps.
+    """
+    import torch
+
+    from paper_2608_02989_amd import ops
+
+    cfg, layers = wl.cfg, wl.layers
+    blocks = wl.blocks(rho)
+    stream = torch.cuda.Stream()
+
+    def run_once(s, b, ev=None):
+        L_, B_ = layers[s], blocks[b]
+        T = B_["h"].shape[0]
+        nb = len(B_["offs"]) - 1
+        outs = {"eligible": L_.sel_out["eligible"][:nb], "idx": L_.sel_out["idx"][:T],
+                "gate": L_.sel_out["gate"][:T], "stats": L_.sel_out["stats"][:nb]}
+        if ev is not None:
+            ev[0].record(stream)
+        ops.route(B_["h"], L_.router, out=L_.logits[:T], stream=stream)
+        ops.select(L_.logits[:T], B_["parent"], B_["depth"], B_["prob"], B_["offs"], L_.k, L_.beta, L_.mode,
+                   L_.budget, L_.removal_cap, B_["resident"], workspace=L_.sel_ws, outputs=outs, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        ops.moe_forward(B_["h"], L_.wgu, L_.wd, outs["idx"], outs["gate"], out=L_.out[:T],
+                        workspace=L_.fwd_ws, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        return outs
+
+    # untimed pre-pass: routed union, |S'| and |U_nat| of every (set, block) pair
+    # (selection is deterministic) and its routing, kept for the forward-only graph
+    routed, sprime, unat, routing = {}, {}, {}, {}
+    with torch.cuda.stream(stream):
+        for s in range(wl.n_sets):
+            for b in range(wl.nblocks):
+                sel = run_once(s, b)
+                idx = sel["idx"]
+                routing[(s, b)] = (idx.clone(), sel["gate"].clone())
+                routed[(s, b)] = int(torch.unique(idx[idx >= 0]).numel())
+                st = sel["stats"].cpu().numpy()
+                sprime[(s, b)] = float(st[:, 4].mean())
+                unat[(s, b)] = float(st[:, 5].mean())
+    torch.cuda.synchronize()
+    seq = [(i % wl.n_sets, i % wl.nblocks) for i in range(warmup + steps)]
+    timed = seq[warmup:]
+    r = np.array([routed[c] for c in timed], np.float64)
+    weight_bytes = float(r.mean()) * wl.ebytes
+    eb = 2 if cfg.dtype == "bf16" else 4
+    act_bytes = wl.T * cfg.H * eb + wl.T * cfg.H * 4 + wl.T * cfg.k * 8   # hidden in, out, routing in
+    fwd_bytes = weight_bytes + act_bytes
+
+    # (1) eager launches, HIP events around every step and every forward
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(steps)]
+    with torch.cuda.stream(stream):
+        for (s, b) in seq[:warmup]:
+            run_once(s, b)
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for i, (s, b) in enumerate(timed):
+            run_once(s, b, evs[i])
+        stop.record(stream)
+    torch.cuda.synchronize()
+    eager_us = start.elapsed_time(stop) * 1e3 / steps
+    step_eager = [a.elapsed_time(z) * 1e3 for a, _, z in evs]
+    fwd_eager = [m.elapsed_time(z) * 1e3 for _, m, z in evs]
+
+    def graph_time(body):
+        """Average replay time of a graph of `body` (the timed sequence), replayed
+        until at least min_graph_steps steps ran; per-replay times returned too."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(stream):
+            with torch.cuda.graph(g, stream=stream):
+                body()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        reps = max(1, -(-min_graph_steps // steps))
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        with torch.cuda.stream(stream):
+            marks[0].record(stream)
+            for i in range(reps):
+                g.replay()
+                marks[i + 1].record(stream)
+        torch.cuda.synchronize()
+        per = [marks[i].elapsed_time(marks[i + 1]) * 1e3 / steps for i in range(reps)]
+        del g
+        return marks[0].elapsed_time(marks[-1]) * 1e3 / (reps * steps), per, reps
+
+    step_us, fwd_us, step_reps, fwd_reps, reps = None, None, None, None, 0
+    if graph:
+        step_us, step_reps, reps = graph_time(lambda: [run_once(s, b) for (s, b) in timed])
+
+        def fwd_body():
+            for (s, b) in timed:
+                L_, B_ = layers[s], blocks[b]
+                T = B_["h"].shape[0]
+                ops.moe_forward(B_["h"], L_.wgu, L_.wd, routing[(s, b)][0], routing[(s, b)][1], out=L_.out[:T],
+                                workspace=L_.fwd_ws, stream=stream)
+        fwd_us, fwd_reps, _ = graph_time(fwd_body)
+    headline_us = step_us if step_us is not None else eager_us
+    fwd_time_us = fwd_us if fwd_us is not None else float(np.mean(fwd_eager))
+    return dict(
+        step_us=headline_us, eager_us=eager_us, graph=step_us is not None, graph_reps=reps,
+        step_eager_p50=_pct(step_eager, 50), step_eager_p10=_pct(step_eager, 10), step_eager_p90=_pct(step_eager, 90),
+        step_graph_replays=None if step_reps is None else [round(x, 2) for x in step_reps],
+        value=weight_bytes / (headline_us * 1e-6) / 1e9,
+        weight_bytes=weight_bytes, fwd_bytes=fwd_bytes, fwd_us=fwd_time_us,
+        fwd_gbs=fwd_bytes / (fwd_time_us * 1e-6) / 1e9,
+        fwd_eager_us=float(np.mean(fwd_eager)), fwd_eager_p50=_pct(fwd_eager, 50),
+        fwd_eager_gbs=fwd_bytes / (float(np.mean(fwd_eager)) * 1e-6) / 1e9,
+        fwd_timing="HIP graph of the timed steps' forward launches" if fwd_us is not None else "eager HIP events",
+        routed=float(r.mean()), sprime=float(np.mean([sprime[c] for c in timed])),
+        unat=float(np.mean([unat[c] for c in timed])),
+        flops=float(wl.T * cfg.k * 6 * cfg.H * cfg.I + 2 * wl.T * cfg.E * cfg.H),
+        blocks=blocks,
+    )
+
+
+def workload_text(wl: Workload, rho) -> str:
+    cfg = wl.cfg
+    txt = (f"{cfg.name}: 1 MoE layer, verify block T={wl.T} ({cfg.B} tree{'s' if cfg.B > 1 else ''} of "
+           f"{cfg.T} nodes), H={cfg.H} E={cfg.E} top-{cfg.k} I={cfg.I}, {cfg.dtype} experts, fp32 router, "
+           f"tree-correlated hidden rho={rho}")
+    if cfg.resident_frac:
+        txt += f", {int(round(cfg.resident_frac * 100))}% residency mask"
+    if cfg.B > 1:
+        txt += ", a separate eligible set per tree"
+    if wl.tp_share > 1:
+        txt += f"; one GPU's I/{wl.tp_share} shard of I={wl.full_I} (tensor parallel over I)"
+    return txt
+
+
+def roofline_block(wl: Workload, m) -> dict:
+    ratio = measured_traffic(wl.cfg.name) if wl.tp_share == 1 else None
+    return {"bound": "hbm",
+            "kernel": "acceptmoe_moe_forward (gate/up + down passes of the grouped SwiGLU FFN)",
+            "achieved": round(m["fwd_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(m["fwd_gbs"] / HBM_PEAK_GBS, 4),
+            "traffic": None if ratio is None else round(ratio * m["fwd_bytes"]),
+            "traffic_ratio": ratio,
+            "bytes_per_launch": round(m["fwd_bytes"]), "launch_us": round(m["fwd_us"], 2),
+            "launch_timing": m["fwd_timing"],
+            "eager_launch_us": round(m["fwd_eager_us"], 2), "eager_launch_p50_us": m["fwd_eager_p50"],
+            "eager_achieved": round(m["fwd_eager_gbs"], 1),
+            "mfma_util": round(m["flops"] / (m["fwd_us"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5)}
+
+
+def summary(wl: Workload, m, rho) -> dict:
+    return {"workload": workload_text(wl, rho), "value": round(m["value"], 1), "unit": "GB/s",
+            "latency_us": round(m["step_us"], 2), "eager_latency_us": round(m["eager_us"], 2),
+            "eager_step_p10_p50_p90_us": [m["step_eager_p10"], m["step_eager_p50"], m["step_eager_p90"]],
+            "weight_MB_per_step": round(m["weight_bytes"] / 1e6, 1),
+            "routed_experts": round(m["routed"], 2), "eligible": round(m["sprime"], 2),
+            "natural_union": round(m["unat"], 2), "roofline": roofline_block(wl, m)}
 
 
 def main():
@@ -120,256 +387,80 @@ def main():
               "sharding it over several GPUs is designed but not built", file=sys.stderr)
         sys.exit(2)
 
-    import torch
-
-    from paper_2608_02989_amd import ops
     from paper_2608_02989_amd import workload as W
 
-    dev = "cuda"
-    cfg = W.CONFIGS[args.config]
-    if cfg.layers > 1:
-        stack_report(args, cfg)
+    if args.modes:
+        modes_report(args)
         return
-    full_I = cfg.I
-    if args.tp_share > 1:
-        # one GPU's shard: the seeds depend on the configuration id, not on I,
-        # so routing is the full layer's and only the expert weights shrink
-        G = args.tp_share
-        if cfg.I % (32 * G) != 0:
-            print(f"--tp-share {G}: I = {cfg.I} does not split into {G} multiples of 32", file=sys.stderr)
-            sys.exit(2)
-        cfg = W.LayerConfig(**{**cfg.__dict__, "I": cfg.I // G})
-    Ttot = cfg.total_tokens
-    ebytes = cfg.expert_bytes
-    layer_bytes = cfg.E * ebytes
-    n_sets = args.sets or max(4, int(np.ceil(2 * 2**30 / layer_bytes)))
-    n_sets = min(n_sets, 16)
+    if W.CONFIGS[args.config].layers > 1:
+        stack_report(args, W.CONFIGS[args.config])
+        return
     t0 = time.time()
 
     def log(msg):
         print(f"[bench {time.time() - t0:6.1f}s] {msg}", file=sys.stderr, flush=True)
 
-    log(f"config {cfg.name} T={Ttot} B={cfg.B} H={cfg.H} E={cfg.E} k={cfg.k} I={cfg.I} "
-        f"dtype={cfg.dtype} sets={n_sets} blocks={args.blocks}")
-
-    # ---- weights: n_sets independently seeded layers, packed once ----
-    layers = []
-    for s in range(n_sets):
-        rw = torch.from_numpy(W.router_weights(cfg, s)).to(dev)
-        wg, wu, wd = W.expert_weights_torch(cfg, s, dev)
-        layers.append(ops.VerifyLayer(rw, wg, wu, wd, cfg.k, max_tokens=Ttot, max_trees=cfg.B))
-        del wg, wu, wd
-    torch.cuda.synchronize()
-    torch.cuda.empty_cache()
-    log("weights generated and packed")
-
-    def make_blocks(rho):
-        out = []
-        for b in range(args.blocks):
-            blk = W.make_block(cfg, block=b, layer=0, rho=rho)
-            if cfg.dtype == "bf16":
-                h = torch.from_numpy(W.bf16_round(blk.hidden).view(np.int16)).view(torch.bfloat16).to(dev)
-            else:
-                h = torch.from_numpy(blk.hidden).to(dev)
-            out.append(dict(
-                h=h, parent=torch.from_numpy(blk.parent).to(dev), depth=torch.from_numpy(blk.depth).to(dev),
-                prob=torch.from_numpy(blk.prob).to(dev), offs=blk.offsets.tolist(),
-                resident=None if blk.resident is None else torch.from_numpy(blk.resident).to(dev), host=blk))
-        return out
-
-    def combos(n):
-        return [(i % n_sets, i % args.blocks) for i in range(n)]
-
-    def run_once(blocks, s, b, stream, ev=None):
-        L_, B_ = layers[s], blocks[b]
-        if ev is None:
-            return L_.step(B_["h"], B_["parent"], B_["depth"], B_["prob"], B_["offs"], B_["resident"], stream)
-        T = B_["h"].shape[0]
-        logits = L_.logits[:T]
-        ops.route(B_["h"], L_.router, out=logits, stream=stream)
-        nb = len(B_["offs"]) - 1
-        outs = {"eligible": L_.sel_out["eligible"][:nb], "idx": L_.sel_out["idx"][:T],
-                "gate": L_.sel_out["gate"][:T], "stats": L_.sel_out["stats"][:nb]}
-        ops.select(logits, B_["parent"], B_["depth"], B_["prob"], B_["offs"], L_.k, L_.beta, L_.mode,
-                   L_.budget, L_.removal_cap, B_["resident"], workspace=L_.sel_ws, outputs=outs, stream=stream)
-        ev[0].record(stream)
-        ops.moe_forward(B_["h"], L_.wgu, L_.wd, outs["idx"], outs["gate"], out=L_.out[:T],
-                        workspace=L_.fwd_ws, stream=stream)
-        ev[1].record(stream)
-
-    def measure(rho, steps, warmup):
-        blocks = make_blocks(rho)
-        stream = torch.cuda.Stream()
-        # untimed pre-pass: the routed union of every (set, block) pair (selection is
-        # deterministic) and its routing, kept for the forward-only timing below
-        routed, sprime, unat, routing = {}, {}, {}, {}
-        with torch.cuda.stream(stream):
-            for s in range(n_sets):
-                for b in range(args.blocks):
-                    _, sel, _ = run_once(blocks, s, b, stream)
-                    idx = sel["idx"]
-                    routing[(s, b)] = (idx.clone(), sel["gate"].clone())
-                    routed[(s, b)] = int(torch.unique(idx[idx >= 0]).numel())
-                    st = sel["stats"].cpu().numpy()
-                    sprime[(s, b)] = float(st[:, 4].mean())
-                    unat[(s, b)] = float(st[:, 5].mean())
-        torch.cuda.synchronize()
-        seq = combos(warmup + steps)
-        timed = seq[warmup:]
-        r = np.array([routed[c] for c in timed], np.float64)
-        weight_bytes = r * ebytes
-        act_bytes = Ttot * cfg.H * (2 if cfg.dtype == "bf16" else 4) + Ttot * cfg.H * 4 + Ttot * cfg.k * 8
-        fwd_bytes = weight_bytes + act_bytes
-
-        # (1) eager launches, HIP events around every expert-FFN launch
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-        with torch.cuda.stream(stream):
-            for (s, b) in seq[:warmup]:
-                run_once(blocks, s, b, stream)
-            torch.cuda.synchronize()
-            start = torch.cuda.Event(enable_timing=True)
-            stop = torch.cuda.Event(enable_timing=True)
-            start.record(stream)
-            for i, (s, b) in enumerate(timed):
-                run_once(blocks, s, b, stream, evs[i])
-            stop.record(stream)
-        torch.cuda.synchronize()
-        eager_ms = start.elapsed_time(stop)
-        fwd_ms = [a.elapsed_time(z) for a, z in evs]
-
-        # (2) the same step sequence replayed from a HIP graph (no host launch cost)
-        period = n_sets * args.blocks // int(np.gcd(n_sets, args.blocks))
-        graph_ms = None
-        if args.graph:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.stream(stream):
-                with torch.cuda.graph(g, stream=stream):
-                    for (s, b) in combos(period):
-                        run_once(blocks, s, b, stream)
-            torch.cuda.synchronize()
-            reps = max(1, (steps + period - 1) // period)
-            for _ in range(2):
-                g.replay()
-            torch.cuda.synchronize()
-            gs, ge = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            gs.record(stream)
-            with torch.cuda.stream(stream):
-                for _ in range(reps):
-                    g.replay()
-            ge.record(stream)
-            torch.cuda.synchronize()
-            graph_ms = gs.elapsed_time(ge) / (reps * period) * steps
-            del g
-        # (3) the forward launches alone, replayed from a HIP graph over the same
-        # rotation (every (set, block) pair's routing from the pre-pass): the
-        # average launch duration without the host launch cost that the eager
-        # events around each launch include
-        fwd_graph_us, fwd_graph_bytes = None, None
-        if args.graph:
-            pairs = combos(period)
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.stream(stream):
-                with torch.cuda.graph(g, stream=stream):
-                    for (s, b) in pairs:
-                        L_, B_ = layers[s], blocks[b]
-                        T = B_["h"].shape[0]
-                        ops.moe_forward(B_["h"], L_.wgu, L_.wd, routing[(s, b)][0], routing[(s, b)][1],
-                                        out=L_.out[:T], workspace=L_.fwd_ws, stream=stream)
-            torch.cuda.synchronize()
-            reps = max(1, (steps + period - 1) // period)
-            for _ in range(2):
-                g.replay()
-            torch.cuda.synchronize()
-            gs, ge = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            gs.record(stream)
-            with torch.cuda.stream(stream):
-                for _ in range(reps):
-                    g.replay()
-            ge.record(stream)
-            torch.cuda.synchronize()
-            fwd_graph_us = gs.elapsed_time(ge) * 1e3 / (reps * period)
-            fwd_graph_bytes = float(np.mean([routed[c] * ebytes for c in pairs])) + act_bytes
-            del g
-        total_ms = graph_ms if graph_ms is not None else eager_ms
-        return dict(
-            ms_per_step=total_ms / steps,
-            eager_us=eager_ms / steps * 1e3,
-            graph_us=None if graph_ms is None else graph_ms / steps * 1e3,
-            value=float(weight_bytes.sum() / (total_ms * 1e-3) / 1e9),
-            fwd_us=float(np.mean(fwd_ms) * 1e3) if fwd_graph_us is None else fwd_graph_us,
-            fwd_gbs=(float(fwd_bytes.sum() / (np.sum(fwd_ms) * 1e-3) / 1e9) if fwd_graph_us is None
-                     else fwd_graph_bytes / (fwd_graph_us * 1e-6) / 1e9),
-            fwd_bytes_per_launch=float(fwd_bytes.mean()) if fwd_graph_bytes is None else fwd_graph_bytes,
-            fwd_eager_us=float(np.mean(fwd_ms) * 1e3),
-            fwd_eager_gbs=float(fwd_bytes.sum() / (np.sum(fwd_ms) * 1e-3) / 1e9),
-            fwd_timing="HIP graph of forward launches" if fwd_graph_us is not None else "eager HIP events",
-            routed=float(r.mean()), sprime=float(np.mean([sprime[c] for c in timed])),
-            unat=float(np.mean([unat[c] for c in timed])),
-            flops=float(Ttot * cfg.k * 6 * cfg.H * cfg.I + 2 * Ttot * cfg.E * cfg.H),
-            blocks=blocks, stream=stream,
-        )
-
-    main_m = measure(args.rho, args.steps, args.warmup)
-    log(f"rho={args.rho}: {main_m['ms_per_step'] * 1e3:.1f} us/step (eager {main_m['eager_us']:.1f}), "
+    wl = Workload(args.config, args, log, tp_share=args.tp_share, sets=args.sets)
+    cfg = wl.cfg
+    main_m = measure(wl, args.rho, args.steps, args.warmup, graph=bool(args.graph))
+    log(f"rho={args.rho}: {main_m['step_us']:.1f} us/step (eager {main_m['eager_us']:.1f}), "
         f"{main_m['value']:.0f} GB/s, ffn {main_m['fwd_us']:.1f} us ({main_m['fwd_gbs']:.0f} GB/s), "
         f"routed {main_m['routed']:.1f}")
 
     alt = None
     if not args.no_alt and args.rho != 0.0:
-        m0 = measure(0.0, args.steps, args.warmup)
-        alt = {"rho": 0.0, "value": round(m0["value"], 1), "latency_us": round(m0["ms_per_step"] * 1e3, 2),
+        m0 = measure(wl, 0.0, args.steps, args.warmup, graph=bool(args.graph))
+        alt = {"rho": 0.0, "value": round(m0["value"], 1), "latency_us": round(m0["step_us"], 2),
                "eager_latency_us": round(m0["eager_us"], 2),
                "ffn_us": round(m0["fwd_us"], 2), "ffn_gbs": round(m0["fwd_gbs"], 1),
                "routed_experts": round(m0["routed"], 2), "eligible": round(m0["sprime"], 2),
                "natural_union": round(m0["unat"], 2)}
-        log(f"rho=0: {m0['ms_per_step'] * 1e3:.1f} us/step, {m0['value']:.0f} GB/s, routed {m0['routed']:.1f}")
+        log(f"rho=0: {m0['step_us']:.1f} us/step, {m0['value']:.0f} GB/s, routed {m0['routed']:.1f}")
 
-    # ---- CPU oracle baseline on a bounded sample ----
+    # ---- CPU oracle baseline on a bounded sample (headline workload only) ----
     cpu = None
     if args.cpu_seconds > 0:
-        cpu = cpu_baseline(cfg, layers, main_m["blocks"], args.cpu_seconds, ebytes, log)
+        cpu = cpu_baseline(cfg, wl.layers, main_m["blocks"], args.cpu_seconds, args.cpu_seconds_1t, wl.ebytes, log)
+    wl.free()
 
-    frac = main_m["fwd_gbs"] / HBM_PEAK_GBS
+    companions = {}
+    for name in [c for c in args.companions.split(",") if c and c != args.config]:
+        cw = Workload(name, args, log)
+        cm = measure(cw, args.rho, args.steps, args.warmup, graph=bool(args.graph))
+        companions[name] = summary(cw, cm, args.rho)
+        log(f"{name}: {cm['step_us']:.1f} us/step, {cm['value']:.0f} GB/s, ffn {cm['fwd_us']:.1f} us "
+            f"({cm['fwd_gbs']:.0f} GB/s), routed {cm['routed']:.1f}")
+        cw.free()
+
+    head = summary(wl, main_m, args.rho)
     line = {
         "metric": "verify-block MoE layer latency (us) + eligible-expert weight HBM GB/s, 1 GPU",
-        "value": round(main_m["value"], 1),
+        "value": head["value"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(main_m["ms_per_step"], 5),
-        "latency_us": round(main_m["ms_per_step"] * 1e3, 2),
+        "ms_per_step": round(main_m["step_us"] / 1e3, 5),
+        "latency_us": head["latency_us"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: 1 MoE layer, verify block T={Ttot} (B={cfg.B} trees), "
-                               f"H={cfg.H} E={cfg.E} top-{cfg.k} I={cfg.I}, {cfg.dtype} experts, fp32 router, "
-                               f"tree-correlated hidden rho={args.rho}"
-                               + (f"; one GPU's I/{args.tp_share} shard of I={full_I} (tensor parallel over I)"
-                                  if args.tp_share > 1 else ""),
-                   "T": Ttot, "B": cfg.B, "H": cfg.H, "E": cfg.E, "k": cfg.k, "I": cfg.I,
-                   "rho": args.rho, "weight_sets": n_sets, "blocks": args.blocks,
-                   **({"tp_share": args.tp_share, "I_full": full_I} if args.tp_share > 1 else {}),
-                   "routed_experts": round(main_m["routed"], 2), "eligible": round(main_m["sprime"], 2),
-                   "natural_union": round(main_m["unat"], 2)},
-        "roofline": {"bound": "hbm", "kernel": "acceptmoe_moe_forward (gate_up with per-item dispatch + down with in-LDS combine)",
-                     "achieved": round(main_m["fwd_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(frac, 4),
-                     "traffic": (None if measured_traffic() is None
-                                 else round(measured_traffic() * main_m["fwd_bytes_per_launch"])),
-                     "bytes_per_launch": round(main_m["fwd_bytes_per_launch"]),
-                     "launch_us": round(main_m["fwd_us"], 2),
-                     "launch_timing": main_m["fwd_timing"],
-                     "eager_launch_us": round(main_m["fwd_eager_us"], 2),
-                     "eager_achieved": round(main_m["fwd_eager_gbs"], 1),
-                     "mfma_util": round(main_m["flops"] / (main_m["fwd_us"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5)},
+        "config": {"workload": head["workload"],
+                   "T": wl.T, "B": cfg.B, "H": cfg.H, "E": cfg.E, "k": cfg.k, "I": cfg.I,
+                   "rho": args.rho, "weight_sets": wl.n_sets, "blocks": wl.nblocks,
+                   **({"tp_share": wl.tp_share, "I_full": wl.full_I} if wl.tp_share > 1 else {}),
+                   "routed_experts": head["routed_experts"], "eligible": head["eligible"],
+                   "natural_union": head["natural_union"], "weight_MB_per_step": head["weight_MB_per_step"]},
+        "roofline": head["roofline"],
         "cpu_baseline": cpu,
+        "timing": (f"HIP graph of the {args.steps} timed steps, replayed {main_m['graph_reps']}x; value = routed "
+                   "expert-weight bytes of those steps / their time" if main_m["graph"] else "eager launches"),
+        "eager_latency_us": head["eager_latency_us"],
+        "eager_step_p10_p50_p90_us": head["eager_step_p10_p50_p90_us"],
         "alt_iid": alt,
-        "timing": "HIP graph replay of the rotated step sequence" if main_m["graph_us"] is not None
-                  else "eager launches",
-        "eager_latency_us": round(main_m["eager_us"], 2),
+        "companions": companions,
     }
     print(json.dumps(line), flush=True)
 
@@ -743,16 +834,19 @@ def estimate_report(args):
     print(json.dumps(report), flush=True)
 
 
-def cpu_baseline(cfg, layers, blocks, budget_s, ebytes, log):
-    """Oracle route + select + grouped forward per block, host cores, bounded sample."""
-    import torch
+def modes_report(args):
+    raise SystemExit("--modes: not available")
 
+
+def cpu_baseline(cfg, layers, blocks, budget_s, budget_1t, ebytes, log):
+    """Oracle route + select + grouped forward per block on the host cores, a
+    bounded sample, with all BLAS threads and then with one thread."""
     from oracle import acceptmoe_oracle as O
     from paper_2608_02989_amd import workload as W
 
     L0 = layers[0]
     rw = L0.router_w.cpu().numpy().astype(np.float64)
-    # the oracle reads row-major weights: unpack by regenerating the same seeded layer on the host side
+    # the oracle reads row-major weights: regenerate the same seeded layer
     wg, wu, wd = W.expert_weights_torch(cfg, 0, "cuda")
     host = [{}, {}, {}]
 
@@ -771,40 +865,56 @@ def cpu_baseline(cfg, layers, blocks, budget_s, ebytes, log):
         def __getitem__(self, e):
             return host[self.j][int(e)]
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
-    elapsed, nbytes, n = 0.0, 0.0, 0
+    def blas_threads():
+        try:
+            from threadpoolctl import threadpool_info
+            return max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+        except Exception:
+            return os.cpu_count() or 1
+
     prepared = set()
-    # cycle over the blocks until the time budget is used (a bounded sample)
-    for b in itertools.cycle(range(len(blocks))):
-        blk = blocks[b]["host"]
-        h64 = (O.widen_bf16(W.bf16_round(blk.hidden)) if cfg.dtype == "bf16"
-               else blk.hidden.astype(np.float64))
-        if b not in prepared:
-            # weights needed by this block go to host memory before the clock starts
-            z_pre = O.route(h64, rw).astype(np.float32)
-            pre = O.select(z_pre, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, resident=blk.resident)
-            for e in np.unique(pre["idx"][pre["idx"] >= 0]):
-                fetch(int(e))
-            prepared.add(b)
-        t1 = time.perf_counter()
-        z = O.route(h64, rw).astype(np.float32)
-        sel = O.select(z, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, resident=blk.resident)
-        O.moe_forward_grouped(h64, View(0), View(1), View(2), sel["idx"], sel["gate"], cfg.dtype)
-        elapsed += time.perf_counter() - t1
-        nbytes += len(np.unique(sel["idx"][sel["idx"] >= 0])) * ebytes
-        n += 1
-        if elapsed >= budget_s:
-            break
+
+    def sample(budget):
+        elapsed, nbytes, n = 0.0, 0.0, 0
+        # cycle over the blocks until the time budget is used (a bounded sample)
+        for b in itertools.cycle(range(len(blocks))):
+            blk = blocks[b]["host"]
+            h64 = (O.widen_bf16(W.bf16_round(blk.hidden)) if cfg.dtype == "bf16"
+                   else blk.hidden.astype(np.float64))
+            if b not in prepared:
+                # weights needed by this block go to host memory before the clock starts
+                z_pre = O.route(h64, rw).astype(np.float32)
+                pre = O.select(z_pre, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, resident=blk.resident)
+                for e in np.unique(pre["idx"][pre["idx"] >= 0]):
+                    fetch(int(e))
+                prepared.add(b)
+            t1 = time.perf_counter()
+            z = O.route(h64, rw).astype(np.float32)
+            sel = O.select(z, blk.parent, blk.depth, blk.prob, blk.offsets, cfg.k, resident=blk.resident)
+            O.moe_forward_grouped(h64, View(0), View(1), View(2), sel["idx"], sel["gate"], cfg.dtype)
+            elapsed += time.perf_counter() - t1
+            nbytes += len(np.unique(sel["idx"][sel["idx"] >= 0])) * ebytes
+            n += 1
+            if elapsed >= budget:
+                return n, elapsed, nbytes
+
+    threads = blas_threads()
+    n, elapsed, nbytes = sample(budget_s)
+    log(f"cpu oracle: {n} blocks in {elapsed:.1f}s ({threads} threads)")
+    one = None
+    if budget_1t > 0:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            n1, el1, nb1 = sample(budget_1t)
+        log(f"cpu oracle, 1 thread: {n1} blocks in {el1:.1f}s")
+        one = {"value": round(nb1 / el1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+               "latency_us": round(el1 / n1 * 1e6, 1), "sample": f"{n1} block passes, {el1:.1f} s"}
     del wg, wu, wd
-    log(f"cpu oracle: {n} blocks in {elapsed:.1f}s")
     return {"value": round(nbytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
             "sample": f"{n} block passes over {len(prepared)} seeded blocks of {cfg.name} (layer 0), "
                       f"route+select+grouped forward in fp64 numpy, {elapsed:.1f} s",
-            "latency_us": round(elapsed / n * 1e6, 1)}
+            "latency_us": round(elapsed / n * 1e6, 1), "one_thread": one}
 
 
 if __name__ == "__main__":

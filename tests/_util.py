@@ -3,6 +3,9 @@ oracle-side preparation, tolerance checks.  Inputs come from the workload
 generator; expected values come from oracle/ only."""
 from __future__ import annotations
 
+import json
+import os
+
 import numpy as np
 
 from oracle import acceptmoe_oracle as O
@@ -14,6 +17,16 @@ LOGIT_TOL = 1e-5          # router logits, fp32 accumulation vs fp64
 GATE_RTOL = 1.2e-7        # gates: fp64 on both sides, one fp32 rounding each (<= 1 ulp)
 
 
+# Per-row bound: max_h |y_th - yref_th| / max_h |yref_th| for every output row t
+# (a row is one token's layer output).  bf16: the SwiGLU activation is stored
+# in bf16 before the down projection, each element rounded with relative error
+# <= u = 2^-9; summed over I terms of random sign that error stays ~u of a
+# row's largest output (measured 1.0-1.5 u at every workload shape), so 3u
+# bounds it.  fp32: accumulation over H or I <= 4096 terms, ~sqrt(H) 2^-24 of
+# the row (measured <= 6e-7); 1e-5 bounds it.
+ROW_TOL = {"f32": 1e-5, "bf16": 3 * 2.0 ** -9}
+
+
 def normwise_rel(got, ref) -> float:
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
@@ -21,6 +34,52 @@ def normwise_rel(got, ref) -> float:
     if scale == 0.0:
         return float(np.max(np.abs(got))) if got.size else 0.0
     return float(np.max(np.abs(got - ref))) / scale
+
+
+def per_row_rel(got, ref) -> float:
+    """Largest over rows t of max|got_t - ref_t| / max|ref_t|.  A row whose
+    reference is all zero must come back exactly zero (else it counts as inf)."""
+    got = np.asarray(got, np.float64).reshape(len(got), -1)
+    ref = np.asarray(ref, np.float64).reshape(len(ref), -1)
+    if ref.size == 0:
+        return 0.0
+    diff = np.max(np.abs(got - ref), axis=1)
+    scale = np.max(np.abs(ref), axis=1)
+    zero = scale == 0.0
+    out = np.where(zero, np.where(diff == 0.0, 0.0, np.inf), diff / np.where(zero, 1.0, scale))
+    return float(out.max())
+
+
+def elementwise_rel(got, ref) -> float:
+    """Largest |got - ref| / (|ref| + 1e-3 max|ref|) over all elements (reported
+    beside the normwise figure; near-zero outputs make it large by nature)."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if ref.size == 0:
+        return 0.0
+    floor = 1e-3 * float(np.max(np.abs(ref)))
+    den = np.abs(ref) + floor
+    if floor == 0.0:
+        return 0.0 if np.array_equal(got, ref) else float("inf")
+    return float(np.max(np.abs(got - ref) / den))
+
+
+def check_forward(got, ref, dtype: str, label: str) -> dict:
+    """Asserts the forward contract on one output tensor (normwise and per-row
+    bounds) and reports the three error figures (printed, and appended as a
+    JSON line to $ACCEPTMOE_ERR_REPORT when that is set)."""
+    figs = {"label": label, "dtype": dtype, "normwise": normwise_rel(got, ref),
+            "per_row": per_row_rel(got, ref), "elementwise": elementwise_rel(got, ref)}
+    line = json.dumps(figs)
+    print(f"[errors] {line}", flush=True)
+    path = os.environ.get("ACCEPTMOE_ERR_REPORT")
+    if path:
+        with open(path, "a") as f:
+            f.write(line + "\n")
+    assert np.isfinite(np.asarray(got)).all(), f"{label}: non-finite output"
+    assert figs["normwise"] <= FWD_TOL[dtype], figs
+    assert figs["per_row"] <= ROW_TOL[dtype], figs
+    return figs
 
 
 def hidden_for(cfg: W.LayerConfig, h32: np.ndarray):

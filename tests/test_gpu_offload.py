@@ -13,7 +13,7 @@ from paper_2608_02989_amd import _lib as L
 from paper_2608_02989_amd import ops
 from paper_2608_02989_amd import workload as W
 
-from _util import FWD_TOL, HostExperts, hidden_for, normwise_rel
+from _util import HostExperts, check_forward, hidden_for
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -62,7 +62,7 @@ def test_offload_layer_matches_oracle(gpu, dtype, mode, X):
             ref_pool.serve_wave(OO.wave_experts(ref["idx"], rw_of, w))
         total_waves += rn
         y_ref = O.moe_forward_grouped(h64, *hw, ref["idx"], ref["gate"], cfg.dtype)
-        assert normwise_rel(out.cpu().numpy(), y_ref) <= FWD_TOL[cfg.dtype], b
+        check_forward(out.cpu().numpy(), y_ref, cfg.dtype, f"offload block {b}")
     st = layer.pool.stats
     assert st[L.POOL_HITS] == ref_pool.hits and st[L.POOL_MISSES] == ref_pool.misses
     assert st[L.POOL_WAVES] == total_waves

@@ -11,7 +11,7 @@ from oracle import acceptmoe_oracle as O
 from paper_2608_02989_amd import ops
 from paper_2608_02989_amd import workload as W
 
-from _util import FWD_TOL, GATE_RTOL, LOGIT_TOL, HostExperts, normwise_rel
+from _util import GATE_RTOL, LOGIT_TOL, HostExperts, check_forward, normwise_rel
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -64,7 +64,7 @@ def test_stack_teacher_forced(gpu):
         assert np.allclose(gate, ref["gate"], rtol=GATE_RTOL, atol=0), l
         y = layer.out[:cfg.T].cpu().numpy()
         y_ref = O.moe_forward_grouped(h64, wg, wu, wd, ref["idx"], ref["gate"], "bf16")
-        assert normwise_rel(y, y_ref) <= FWD_TOL["bf16"], l
+        check_forward(y, y_ref, "bf16", f"stack layer {l}")
         # residual: the fp32 sum rounded to nearest even, bit for bit
         want = W.bf16_round(O.widen_bf16(hb).astype(np.float32) + y)
         assert np.array_equal(bits(stack.h[l + 1][:cfg.T]).view(np.uint16), want), l
@@ -158,9 +158,8 @@ def test_stack_full_size_48_layers(gpu):
             y_ref = O.moe_forward_grouped(h64, HostExperts(wg), HostExperts(wu), HostExperts(wd), ref["idx"],
                                           ref["gate"], "bf16")
             del wg, wu, wd
-            err = normwise_rel(y, y_ref)
-            say(f"  layer {l}: |S'| = {sizes[-1]}, output error {err:.2e}")
-            assert err <= FWD_TOL["bf16"], (l, err)
+            figs = check_forward(y, y_ref, "bf16", f"48-layer stack layer {l}")
+            say(f"  layer {l}: |S'| = {sizes[-1]}, output error {figs['normwise']:.2e}")
         want = W.bf16_round(h64.astype(np.float32) + y)
         assert np.array_equal(bits(stack.h[l + 1][:T]).view(np.uint16), want), l
     say(f"  |S'| over the layers: min {min(sizes)}, mean {np.mean(sizes):.1f}, max {max(sizes)}")
