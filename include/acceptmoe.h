@@ -80,6 +80,9 @@ extern "C" {
 #define ACCEPTMOE_MAX_TOPK 32
 #define ACCEPTMOE_MAX_TREES 256
 #define ACCEPTMOE_MAX_TREE_NODES 1024
+/* static scratch of acceptmoe_select_noalloc per device: 8 MiB (e.g. up to
+ * 7,000 nodes at E = 128, k = 8; acceptmoe_select_workspace_size gives the need) */
+#define ACCEPTMOE_SELECT_NOALLOC_MAX_WORKSPACE ((size_t)8 << 20)
 
 /*
  * acceptmoe_packed_router_bytes -- bytes of a packed router matrix:
@@ -173,6 +176,32 @@ int32_t acceptmoe_select(const float* logits, const int32_t* parent, const int32
                          int32_t budget, int32_t removal_cap, const uint8_t* resident_mask,
                          uint8_t* eligible, int32_t* topk_idx, float* topk_gate, int32_t* stats,
                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * acceptmoe_select_noalloc -- acceptmoe_select without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).  The same
+ * kernels and outputs; their scratch is a static device array of
+ * ACCEPTMOE_SELECT_NOALLOC_MAX_WORKSPACE bytes that every device the library
+ * runs on holds from module load until the process ends.  The call allocates
+ * nothing and calls no allocating routine.
+ *
+ *   Arguments as acceptmoe_select.  The scratch of the current device is used;
+ *   `stream` must belong to that device (else ACCEPTMOE_ERR_INVALID_ARG).
+ *   Calls needing more than the maximum (acceptmoe_select_workspace_size(T, E,
+ *   k) > ACCEPTMOE_SELECT_NOALLOC_MAX_WORKSPACE) return ACCEPTMOE_ERR_UNSUPPORTED
+ *   before any HIP call.
+ *   Every call on one device shares that device's array, which keeps the last
+ *   call's contents (each call writes every scratch word it reads before
+ *   reading it, so nothing needs clearing); calls that overlap on one device,
+ *   e.g. on two streams, race and are not allowed.
+ */
+int32_t acceptmoe_select_noalloc(const float* logits, const int32_t* parent, const int32_t* depth,
+                                 const float* commit_prob, const int32_t* tree_offsets, int32_t B,
+                                 int32_t T, int32_t E, int32_t k, double beta, int32_t mode,
+                                 int32_t budget, int32_t removal_cap, const uint8_t* resident_mask,
+                                 uint8_t* eligible, int32_t* topk_idx, float* topk_gate, int32_t* stats,
+                                 void* stream);
 
 /*
  * acceptmoe_packed_weights_bytes -- bytes of a packed expert-weight stack.

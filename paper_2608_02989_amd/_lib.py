@@ -34,6 +34,7 @@ MAX_EXPERTS = 512
 MAX_TOPK = 32
 MAX_TREES = 256
 MAX_TREE_NODES = 1024
+SELECT_NOALLOC_MAX_WORKSPACE = 8 << 20
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -47,6 +48,8 @@ SIGNATURES = {
     "acceptmoe_select": (_i32, [_vp, _vp, _vp, _vp, ctypes.POINTER(_i32), _i32, _i32, _i32, _i32,
                                 ctypes.c_double, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
                                 _vp]),
+    "acceptmoe_select_noalloc": (_i32, [_vp, _vp, _vp, _vp, ctypes.POINTER(_i32), _i32, _i32, _i32, _i32,
+                                        ctypes.c_double, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
     "acceptmoe_packed_weights_bytes": (_sz, [_i32, _i32, _i32, _i32]),
     "acceptmoe_pack_expert_weights": (_i32, [_vp, _i32, _i32, _i32, _i32, _vp, _vp]),
     "acceptmoe_moe_forward_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),

@@ -17,6 +17,76 @@ using amoe::abi::clear_err;
 using amoe::abi::fail;
 using amoe::abi::hip_fail;
 
+namespace amoe {
+
+// Host checks of a selection call (no HIP call, no pointer dereferenced
+// except the host tree_offsets); fills the kernel parameters and the tree
+// offsets.  `noop` is set for an empty call (T == 0 and B == 0).
+int32_t select_prepare(const char* who, const float* logits, const int32_t* parent, const int32_t* depth,
+                       const float* commit_prob, const int32_t* tree_offsets, int32_t B, int32_t T, int32_t E,
+                       int32_t k, double beta, int32_t mode, int32_t budget, int32_t removal_cap,
+                       const uint8_t* resident_mask, uint8_t* eligible, int32_t* topk_idx, float* topk_gate,
+                       int32_t* stats, SelectParams& p, TreeOffsets& offs, bool& noop) {
+  noop = false;
+  if (T < 0) return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: T must be >= 0 (got %d)", who, T);
+  if (T == 0 && B == 0) {
+    noop = true;
+    return ACCEPTMOE_OK;
+  }
+  if (E < 1 || E > ACCEPTMOE_MAX_EXPERTS)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "%s: E must be in [1, %d] (got %d)", who, ACCEPTMOE_MAX_EXPERTS, E);
+  if (k < 1 || k > E || k > ACCEPTMOE_MAX_TOPK)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "%s: k must be in [1, min(E, %d)] (got k=%d, E=%d)", who,
+                ACCEPTMOE_MAX_TOPK, k, E);
+  if (B < 1 || B > ACCEPTMOE_MAX_TREES)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "%s: B must be in [1, %d] (got %d)", who, ACCEPTMOE_MAX_TREES, B);
+  if (!std::isfinite(beta) || beta < 0.0)
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: beta must be finite and >= 0", who);
+  if (mode < ACCEPTMOE_MODE_SELF_SIZING || mode > ACCEPTMOE_MODE_COUNT)
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: unknown mode %d", who, mode);
+  if (tree_offsets == nullptr) {
+    if (B != 1) return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: tree_offsets is NULL but B = %d", who, B);
+    offs.o[0] = 0;
+    offs.o[1] = T;
+  } else {
+    if (tree_offsets[0] != 0) return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: tree_offsets[0] must be 0", who);
+    for (int b = 0; b <= B; ++b) offs.o[b] = tree_offsets[b];
+    for (int b = 0; b < B; ++b) {
+      if (offs.o[b + 1] < offs.o[b])
+        return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: tree_offsets must be non-decreasing", who);
+    }
+    if (offs.o[B] != T) return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: tree_offsets[B] must equal T", who);
+  }
+  for (int b = 0; b < B; ++b)
+    if (offs.o[b + 1] - offs.o[b] > ACCEPTMOE_MAX_TREE_NODES)
+      return fail(ACCEPTMOE_ERR_UNSUPPORTED, "%s: tree %d has more than %d nodes", who, b,
+                  ACCEPTMOE_MAX_TREE_NODES);
+  if (!eligible) return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: null eligible", who);
+  if (T > 0 && (!logits || !depth || !commit_prob || !topk_idx || !topk_gate))
+    return fail(ACCEPTMOE_ERR_INVALID_ARG, "%s: null pointer", who);
+  std::memset(&p, 0, sizeof p);
+  p.logits = logits;
+  p.parent = parent;
+  p.depth = depth;
+  p.prob = commit_prob;
+  p.resident = resident_mask;
+  p.eligible = eligible;
+  p.topk_idx = topk_idx;
+  p.topk_gate = topk_gate;
+  p.stats = stats;
+  p.beta = beta;
+  p.T = T;
+  p.E = E;
+  p.k = k;
+  p.B = B;
+  p.mode = mode;
+  p.budget = budget;
+  p.removal_cap = removal_cap < 0 ? E : removal_cap;
+  return ACCEPTMOE_OK;
+}
+
+}  // namespace amoe
+
 extern "C" {
 
 const char* acceptmoe_last_error(void) { return amoe::abi::g_err; }
@@ -78,65 +148,18 @@ int32_t acceptmoe_select(const float* logits, const int32_t* parent, const int32
                          int32_t* topk_idx, float* topk_gate, int32_t* stats, void* workspace,
                          size_t workspace_bytes, void* stream) {
   clear_err();
-  if (T < 0) return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: T must be >= 0 (got %d)", T);
-  if (T == 0 && B == 0) return ACCEPTMOE_OK;
-  if (E < 1 || E > ACCEPTMOE_MAX_EXPERTS)
-    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "select: E must be in [1, %d] (got %d)", ACCEPTMOE_MAX_EXPERTS, E);
-  if (k < 1 || k > E || k > ACCEPTMOE_MAX_TOPK)
-    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "select: k must be in [1, min(E, %d)] (got k=%d, E=%d)",
-                ACCEPTMOE_MAX_TOPK, k, E);
-  if (B < 1 || B > ACCEPTMOE_MAX_TREES)
-    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "select: B must be in [1, %d] (got %d)", ACCEPTMOE_MAX_TREES, B);
-  if (!std::isfinite(beta) || beta < 0.0)
-    return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: beta must be finite and >= 0");
-  if (mode < ACCEPTMOE_MODE_SELF_SIZING || mode > ACCEPTMOE_MODE_COUNT)
-    return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: unknown mode %d", mode);
+  amoe::SelectParams p;
   amoe::TreeOffsets offs;
-  if (tree_offsets == nullptr) {
-    if (B != 1) return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: tree_offsets is NULL but B = %d", B);
-    offs.o[0] = 0;
-    offs.o[1] = T;
-  } else {
-    if (tree_offsets[0] != 0) return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: tree_offsets[0] must be 0");
-    for (int b = 0; b <= B; ++b) offs.o[b] = tree_offsets[b];
-    for (int b = 0; b < B; ++b) {
-      if (offs.o[b + 1] < offs.o[b])
-        return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: tree_offsets must be non-decreasing");
-    }
-    if (offs.o[B] != T) return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: tree_offsets[B] must equal T");
-  }
-  for (int b = 0; b < B; ++b)
-    if (offs.o[b + 1] - offs.o[b] > ACCEPTMOE_MAX_TREE_NODES)
-      return fail(ACCEPTMOE_ERR_UNSUPPORTED, "select: tree %d has more than %d nodes", b,
-                  ACCEPTMOE_MAX_TREE_NODES);
-  if (!eligible) return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: null eligible");
-  if (T > 0 && (!logits || !depth || !commit_prob || !topk_idx || !topk_gate))
-    return fail(ACCEPTMOE_ERR_INVALID_ARG, "select: null pointer");
+  bool noop = false;
+  const int32_t rc = amoe::select_prepare("select", logits, parent, depth, commit_prob, tree_offsets, B, T, E, k,
+                                          beta, mode, budget, removal_cap, resident_mask, eligible, topk_idx,
+                                          topk_gate, stats, p, offs, noop);
+  if (rc != ACCEPTMOE_OK || noop) return rc;
   const size_t need = amoe::select_workspace_bytes(T, E, k);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need))
     return fail(ACCEPTMOE_ERR_WORKSPACE, "select: workspace needs %zu bytes (got %zu)", need, workspace_bytes);
   if (workspace && !aligned(workspace, 256))
     return fail(ACCEPTMOE_ERR_WORKSPACE, "select: workspace must be 256-byte aligned");
-
-  amoe::SelectParams p;
-  std::memset(&p, 0, sizeof p);
-  p.logits = logits;
-  p.parent = parent;
-  p.depth = depth;
-  p.prob = commit_prob;
-  p.resident = resident_mask;
-  p.eligible = eligible;
-  p.topk_idx = topk_idx;
-  p.topk_gate = topk_gate;
-  p.stats = stats;
-  p.beta = beta;
-  p.T = T;
-  p.E = E;
-  p.k = k;
-  p.B = B;
-  p.mode = mode;
-  p.budget = budget;
-  p.removal_cap = removal_cap < 0 ? E : removal_cap;
   amoe::select_carve(workspace, T, E, k, p);
   hipError_t e = amoe::launch_select(p, offs, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "select launch");

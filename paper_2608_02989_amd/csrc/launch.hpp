@@ -45,6 +45,13 @@ struct SelectParams {
 };
 
 size_t select_workspace_bytes(int T, int E, int k);
+// host checks of acceptmoe_select and its allocation-free variant (api.cpp);
+// returns an acceptmoe status, sets noop for an empty call
+int32_t select_prepare(const char* who, const float* logits, const int32_t* parent, const int32_t* depth,
+                       const float* commit_prob, const int32_t* tree_offsets, int32_t B, int32_t T, int32_t E,
+                       int32_t k, double beta, int32_t mode, int32_t budget, int32_t removal_cap,
+                       const uint8_t* resident_mask, uint8_t* eligible, int32_t* topk_idx, float* topk_gate,
+                       int32_t* stats, SelectParams& p, TreeOffsets& offs, bool& noop);
 void select_carve(void* ws, int T, int E, int k, SelectParams& p);
 hipError_t launch_select(const SelectParams& p, const TreeOffsets& offs, hipStream_t stream);
 hipError_t launch_commit_expand(const float* p_hat, int D, const int32_t* depth, int T, float* prob,

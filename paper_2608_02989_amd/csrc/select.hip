@@ -24,6 +24,9 @@
 // remain above the prefix), keys above it are taken, equal keys are taken
 // lowest expert index first.  This matches the rank definition "fewer than k
 // experts beat e" exactly, ties included.
+#include <mutex>
+
+#include "abi_util.hpp"
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -945,3 +948,83 @@ hipError_t launch_select(const SelectParams& p, const TreeOffsets& offs, hipStre
 }
 
 }  // namespace amoe
+
+// ---------------------------------------------------------------------------
+// Allocation-free selection: the same kernels with their scratch in a static
+// device array instead of a caller workspace.  Each device holds its own copy
+// of the array (module load) until the process ends; its address is looked up
+// once per device, with that device current, and only that address is passed
+// to kernels (the array's name is a host-side stand-in in host code).
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kNoallocScratchBytes = ACCEPTMOE_SELECT_NOALLOC_MAX_WORKSPACE;
+static_assert(kNoallocScratchBytes % 256 == 0, "scratch size keeps 256-byte carving");
+
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// device address of `scratch` on the device the stream runs on (which must be
+// the current device)
+int32_t scratch_address(hipStream_t stream, void** out) {
+  using amoe::abi::fail;
+  using amoe::abi::hip_fail;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "select_noalloc: hipGetDevice");
+  if (stream != nullptr) {
+    hipDevice_t sdev = 0;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return hip_fail(e, "select_noalloc: hipStreamGetDevice");
+    if (static_cast<int>(sdev) != dev)
+      return fail(ACCEPTMOE_ERR_INVALID_ARG, "select_noalloc: the stream belongs to device %d, device %d is current",
+                  static_cast<int>(sdev), dev);
+  }
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "select_noalloc: device index %d beyond %d", dev, kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "select_noalloc: hipGetSymbolAddress(scratch)");
+    if (ptr == nullptr) return fail(ACCEPTMOE_ERR_HIP, "select_noalloc: null scratch address");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return ACCEPTMOE_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t acceptmoe_select_noalloc(const float* logits, const int32_t* parent, const int32_t* depth,
+                                            const float* commit_prob, const int32_t* tree_offsets, int32_t B,
+                                            int32_t T, int32_t E, int32_t k, double beta, int32_t mode,
+                                            int32_t budget, int32_t removal_cap, const uint8_t* resident_mask,
+                                            uint8_t* eligible, int32_t* topk_idx, float* topk_gate,
+                                            int32_t* stats, void* stream) {
+  using amoe::abi::fail;
+  using amoe::abi::hip_fail;
+  amoe::abi::clear_err();
+  amoe::SelectParams p;
+  amoe::TreeOffsets offs;
+  bool noop = false;
+  int32_t rc = amoe::select_prepare("select_noalloc", logits, parent, depth, commit_prob, tree_offsets, B, T, E, k,
+                                    beta, mode, budget, removal_cap, resident_mask, eligible, topk_idx, topk_gate,
+                                    stats, p, offs, noop);
+  if (rc != ACCEPTMOE_OK || noop) return rc;
+  const size_t need = amoe::select_workspace_bytes(T, E, k);
+  if (need > kNoallocScratchBytes)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED,
+                "select_noalloc: T=%d E=%d k=%d needs %zu bytes of scratch, beyond the static %zu bytes "
+                "(use acceptmoe_select with a workspace)", T, E, k, need, kNoallocScratchBytes);
+  void* ws = nullptr;
+  rc = scratch_address(static_cast<hipStream_t>(stream), &ws);
+  if (rc != ACCEPTMOE_OK) return rc;
+  amoe::select_carve(ws, T, E, k, p);
+  hipError_t e = amoe::launch_select(p, offs, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "select_noalloc launch");
+}
+

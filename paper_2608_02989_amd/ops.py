@@ -128,6 +128,41 @@ def select(logits: torch.Tensor, parent: torch.Tensor | None, depth: torch.Tenso
     return outputs
 
 
+def select_noalloc(logits: torch.Tensor, parent: torch.Tensor | None, depth: torch.Tensor, prob: torch.Tensor,
+                   tree_offsets=None, k: int = 8, beta: float = 0.5, mode: int = L.MODE_SELF_SIZING,
+                   budget: int = 0, removal_cap: int = -1, resident: torch.Tensor | None = None,
+                   outputs: dict | None = None, stream=None) -> dict:
+    """select() through acceptmoe_select_noalloc: no workspace, the library's
+    static per-device scratch (calls on one device must not overlap)."""
+    _need(logits, "logits", torch.float32, 2)
+    _need(depth, "depth", torch.int32, 1)
+    _need(prob, "prob", torch.float32, 1)
+    if parent is not None:
+        _need(parent, "parent", torch.int32, 1)
+    if resident is not None:
+        _need(resident, "resident", torch.uint8, 1)
+    T, E = logits.shape
+    if tree_offsets is None:
+        offs_arr, B = None, 1
+    else:
+        offs_np = np.ascontiguousarray(np.asarray(tree_offsets, dtype=np.int32))
+        B = len(offs_np) - 1
+        offs_arr = (ctypes.c_int32 * len(offs_np))(*offs_np.tolist())
+    dev = logits.device
+    if outputs is None:
+        outputs = {
+            "eligible": torch.empty((max(B, 1), E), dtype=torch.uint8, device=dev),
+            "idx": torch.empty((T, k), dtype=torch.int32, device=dev),
+            "gate": torch.empty((T, k), dtype=torch.float32, device=dev),
+            "stats": torch.empty((max(B, 1), L.NUM_STATS), dtype=torch.int32, device=dev),
+        }
+    check(lib().acceptmoe_select_noalloc(
+        _ptr(logits), _ptr(parent), _ptr(depth), _ptr(prob), offs_arr, B, T, E, k, float(beta), int(mode),
+        int(budget), int(removal_cap), _ptr(resident), _ptr(outputs["eligible"]), _ptr(outputs["idx"]),
+        _ptr(outputs["gate"]), _ptr(outputs["stats"]), _stream_ptr(stream)))
+    return outputs
+
+
 def pack_expert_weights(w: torch.Tensor, stream=None) -> torch.Tensor:
     """[E, N, K] row-major stack -> packed MFMA fragment layout (same shape and size)."""
     _need(w, "w", dim=3)

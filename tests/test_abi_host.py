@@ -127,6 +127,47 @@ def test_select_rejects():
     assert sel(T=0, B=0) == L.OK
 
 
+def sel_noalloc(**kw):
+    a = dict(logits=FAKE, parent=FAKE, depth=FAKE, prob=FAKE, offs=None, B=1, T=8, E=16, k=2, beta=0.5,
+             mode=0, budget=0, cap=-1, res=None, elig=FAKE, idx=FAKE, gate=FAKE, stats=FAKE)
+    a.update(kw)
+    offs = a["offs"]
+    offs_arr = None if offs is None else (ctypes.c_int32 * len(offs))(*offs)
+    return L.lib().acceptmoe_select_noalloc(a["logits"], a["parent"], a["depth"], a["prob"], offs_arr, a["B"],
+                                            a["T"], a["E"], a["k"], a["beta"], a["mode"], a["budget"], a["cap"],
+                                            a["res"], a["elig"], a["idx"], a["gate"], a["stats"], None)
+
+
+# the allocation-free variant runs the same host checks, and refuses a call whose
+# scratch need exceeds its static array, all before any HIP call
+def test_select_noalloc_rejects():
+    assert sel_noalloc(k=17) == L.ERR_UNSUPPORTED
+    assert sel_noalloc(T=-3) == L.ERR_INVALID_ARG
+    assert sel_noalloc(B=2, offs=[0, 4, 7]) == L.ERR_INVALID_ARG
+    assert sel_noalloc(elig=None) == L.ERR_INVALID_ARG
+    assert sel_noalloc(beta=float("inf")) == L.ERR_INVALID_ARG
+    assert sel_noalloc(T=0, B=0) == L.OK
+    # 256 trees of 1000 nodes at E = 512: far beyond the static scratch
+    T, E, k = 256 * 1000, 512, 8
+    need = L.lib().acceptmoe_select_workspace_size(T, E, k)
+    assert need > L.SELECT_NOALLOC_MAX_WORKSPACE
+    rc, msg = status_and_msg(sel_noalloc(T=T, E=E, k=k, B=256, offs=[1000 * b for b in range(257)]))
+    assert rc == L.ERR_UNSUPPORTED and "scratch" in msg, msg
+    # the largest single block that still fits at E = 128, k = 8 is refused one node later
+    lo, hi = 1, 200_000
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        if L.lib().acceptmoe_select_workspace_size(mid, 128, 8) <= L.SELECT_NOALLOC_MAX_WORKSPACE:
+            lo = mid
+        else:
+            hi = mid - 1
+    assert lo >= 7000
+    T2 = lo + 1
+    offs = [min(1000 * b, T2) for b in range((T2 + 999) // 1000)] + [T2]
+    rc, msg = status_and_msg(sel_noalloc(T=T2, E=128, k=8, B=len(offs) - 1, offs=offs))
+    assert rc == L.ERR_UNSUPPORTED and "scratch" in msg, msg
+
+
 def test_pack_rejects():
     f = L.lib().acceptmoe_pack_expert_weights
     assert f(FAKE, L.BF16, 2, 24, 64, V(0x900000), None) == L.ERR_UNSUPPORTED     # N % 16
