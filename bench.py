@@ -71,6 +71,8 @@ def parse():
     ap.add_argument("--modes", action="store_true",
                     help="selector modes at a matched budget B_0 (AcceptMoE, AcceptMoE-B, MoE-Spec, Count-B, "
                          "natural routing): set sizes, routed experts and bytes, step latency")
+    ap.add_argument("--modes-configs", default="qwen3_30b_a3b,wide_offload",
+                    help="workloads of the --modes report")
     ap.add_argument("--tp-share", type=int, default=1, metavar="G",
                     help="time one GPU's share of a G-way tensor-parallel split over I: the same routing "
                          "(router, hidden states and trees as the full layer), experts with I/G rows")
@@ -245,7 +247,7 @@ def measure(wl: Workload, rho, steps, warmup, graph=True, min_graph_steps=100):
 
     # untimed pre-pass: routed union, |S'| and |U_nat| of every (set, block) pair
     # (selection is deterministic) and its routing, kept for the forward-only graph
-    routed, sprime, unat, routing = {}, {}, {}, {}
+    routed, ssize, sprime, unat, routing = {}, {}, {}, {}, {}
     with torch.cuda.stream(stream):
         for s in range(wl.n_sets):
             for b in range(wl.nblocks):
@@ -254,6 +256,7 @@ def measure(wl: Workload, rho, steps, warmup, graph=True, min_graph_steps=100):
                 routing[(s, b)] = (idx.clone(), sel["gate"].clone())
                 routed[(s, b)] = int(torch.unique(idx[idx >= 0]).numel())
                 st = sel["stats"].cpu().numpy()
+                ssize[(s, b)] = float(st[:, 3].mean())
                 sprime[(s, b)] = float(st[:, 4].mean())
                 unat[(s, b)] = float(st[:, 5].mean())
     torch.cuda.synchronize()
@@ -326,7 +329,8 @@ def measure(wl: Workload, rho, steps, warmup, graph=True, min_graph_steps=100):
         fwd_eager_us=float(np.mean(fwd_eager)), fwd_eager_p50=_pct(fwd_eager, 50),
         fwd_eager_gbs=fwd_bytes / (float(np.mean(fwd_eager)) * 1e-6) / 1e9,
         fwd_timing="HIP graph of the timed steps' forward launches" if fwd_us is not None else "eager HIP events",
-        routed=float(r.mean()), sprime=float(np.mean([sprime[c] for c in timed])),
+        routed=float(r.mean()), s_size=float(np.mean([ssize[c] for c in timed])),
+        sprime=float(np.mean([sprime[c] for c in timed])),
         unat=float(np.mean([unat[c] for c in timed])),
         flops=float(wl.T * cfg.k * 6 * cfg.H * cfg.I + 2 * wl.T * cfg.E * cfg.H),
         blocks=blocks,
@@ -835,7 +839,54 @@ def estimate_report(args):
 
 
 def modes_report(args):
-    raise SystemExit("--modes: not available")
+    """Selector rules at a matched budget (Sec. 4 baselines): natural routing
+    (Standard SD), AcceptMoE (self-sizing), and at B_0 = the round-half-up mean
+    of AcceptMoE's |S| over the same blocks (Sec. 4's budget rule) the
+    fixed-budget rules AcceptMoE-B (anchor + utility), MoE-Spec (summed router
+    mass) and Count-B (natural votes).  Per rule: mean |S|, |S'|, routed experts,
+    routed weight bytes and the graph-replayed step time over the same timed
+    step sequence.  With the residency mask (wide_offload) AcceptMoE and
+    AcceptMoE-B prune against it; the baselines do not (they are evaluated at
+    full residency)."""
+    from paper_2608_02989_amd import _lib as L
+
+    t0 = time.time()
+
+    def log(msg):
+        print(f"[modes {time.time() - t0:6.1f}s] {msg}", file=sys.stderr, flush=True)
+
+    rules = [("standard_sd", L.MODE_ALL_EXPERTS), ("acceptmoe", L.MODE_SELF_SIZING),
+             ("acceptmoe_b", L.MODE_FIXED_BUDGET), ("moe_spec", L.MODE_MOESPEC), ("count_b", L.MODE_COUNT)]
+    report = {"report": "selector rules at a matched budget B_0", "steps": args.steps, "warmup": args.warmup,
+              "blocks": args.blocks, "configs": {}}
+    for name in [c for c in args.modes_configs.split(",") if c]:
+        wl = Workload(name, args, log)
+        per_cfg = {"workload": workload_text(wl, args.rho), "expert_MB": round(wl.ebytes / 1e6, 3)}
+        for rho in (args.rho, 0.0):
+            for ly in wl.layers:
+                ly.mode, ly.budget = L.MODE_SELF_SIZING, 0
+            base = measure(wl, rho, args.steps, args.warmup, graph=bool(args.graph))
+            mean_s = base["s_size"]
+            b0 = int(np.floor(mean_s + 0.5))
+            rows = {}
+            for rule, mode in rules:
+                for ly in wl.layers:
+                    ly.mode, ly.budget = mode, (b0 if mode >= L.MODE_FIXED_BUDGET else 0)
+                m = base if mode == L.MODE_SELF_SIZING else measure(wl, rho, args.steps, args.warmup,
+                                                                   graph=bool(args.graph))
+                rows[rule] = {"S": round(m["s_size"], 2), "S_prime": round(m["sprime"], 2),
+                              "routed": round(m["routed"], 2), "routed_MB": round(m["weight_bytes"] / 1e6, 1),
+                              "step_us": round(m["step_us"], 2), "forward_us": round(m["fwd_us"], 2),
+                              "weight_GBs": round(m["value"], 1)}
+                log(f"{name} rho={rho} {rule}: {rows[rule]}")
+            per_cfg[f"rho={rho}"] = {"B0": b0, "acceptmoe_mean_S": round(mean_s, 3),
+                                     "natural_union": round(base["unat"], 2), "rules": rows}
+        for ly in wl.layers:
+            ly.mode, ly.budget = L.MODE_SELF_SIZING, 0
+        report["configs"][name] = per_cfg
+        wl.free()
+    report["data"] = "synthetic"
+    print(json.dumps(report), flush=True)
 
 
 def cpu_baseline(cfg, layers, blocks, budget_s, budget_1t, ebytes, log):
