@@ -116,19 +116,21 @@ __device__ __forceinline__ int scan_experts(const int* cnt, int* off, int* activ
   return abase;
 }
 
-// Down-pass items (expert, first CSR row, rows) per 16-token block of each
-// active expert, in active-expert order, and their count (one wave).
+// Down-pass items (expert, first CSR row, rows) per block of p.item_rows
+// tokens of each active expert, in active-expert order, and their count (one
+// wave).
 __device__ __forceinline__ void write_down_items(const ForwardParams& p, const int* cnt, const int* off,
                                                  const int* active, int na, int tid) {
+  const int ir = p.item_rows;
   int base = 0;
   for (int a0 = 0; a0 < na; a0 += kWave) {
     const int a = a0 + tid;
     const int e = a < na ? active[a] : 0;
     const int c = a < na ? cnt[e] : 0;
-    const int nb = (c + 15) / 16;
+    const int nb = (c + ir - 1) / ir;
     const int incl = wave_incl_scan_i32(nb);
     for (int m = 0; m < nb; ++m)
-      p.items[base + incl - nb + m] = make_int4(e, off[e] + 16 * m, min(16, c - 16 * m), 0);
+      p.items[base + incl - nb + m] = make_int4(e, off[e] + ir * m, min(ir, c - ir * m), 0);
     base += lane_value(incl, kWave - 1);
   }
   if (tid == 0) *p.n_items = base;
@@ -881,12 +883,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MTMAX <= 2 
 // ---------------------------------------------------------------------------
 // Column-tile down pass (blocks of up to kColMaxT tokens).  A workgroup owns
 // NB adjacent 16-column tiles of H and one of `ksplit` (1 or 2) parts of I.
-// It streams those tiles' rows of W_d for every down item (expert e, 16-token
-// block of e's list): the items are dealt round-robin to the waves, and each
-// wave runs one continuous two-stage load pipeline across its items.  After
-// an item's last stage the wave adds gate * (act_e W_d^T) into its own LDS
-// accumulator out_w[t, 16 NB columns] (a token appears once per expert, so the
-// lanes of one item never collide).  At the end the waves' accumulators are
+// It streams those tiles' rows of W_d for every down item (expert e, block of
+// up to 16 MTI tokens of e's list): the items are dealt round-robin to the
+// waves, and each wave runs one continuous two-stage load pipeline across its
+// items.  The MTI M-tiles of an item share every weight fragment, so an
+// expert's slice of W_d is streamed once per 16 MTI tokens (an expert with 17
+// to 32 tokens took two passes over it with 16-token items; the second mostly
+// from L2, yet the pass ran at 4.6 instead of 5.9 TB/s).  A second M-tile with
+// no token reads a valid row again (a cache hit); its products are dropped.
+// After an item's last stage the wave adds gate * (act_e W_d^T) into its own
+// LDS accumulator out_w[t, 16 NB columns] (a token appears once per expert, so
+// the lanes of one item never collide).  At the end the waves' accumulators are
 // summed in wave order and written to out, or added into the zeroed out when
 // I is split in two (two fp32 additions onto zero commute, so the result
 // does not depend on which half lands first).  Every workgroup does the same
@@ -906,7 +913,7 @@ struct ColShared {
   int4 items[kColMaxItems];
 };
 
-template <class P, int kU, int NB>
+template <class P, int kU, int NB, int MTI>
 __global__ __launch_bounds__(kColLanes / NB * kWave) void down_col_kernel(ForwardParams p, int ksplit) {
   constexpr int kWaves = kColLanes / NB;
   constexpr int kThreads = kWaves * kWave;
@@ -961,42 +968,55 @@ __global__ __launch_bounds__(kColLanes / NB * kWave) void down_col_kernel(Forwar
       fetch(c);
     }
   };
-  uint4 w0[kU][NB], x0[kU], w1[kU][NB], x1[kU];
-  auto load = [&](uint4 (&wv)[kU][NB], uint4 (&xv)[kU], const Cursor& c) {
+  uint4 w0[kU][NB], x0[kU][MTI], w1[kU][NB], x1[kU][MTI];
+  auto load = [&](uint4 (&wv)[kU][NB], uint4 (&xv)[kU][MTI], const Cursor& c) {
     const int kc = kc0 + c.q * kU;
-    const uint4* xp = act + static_cast<size_t>(c.row0 + min(r, c.nrows - 1)) * rowq + g + kc * 4;
+    const uint4* xp[MTI];
+#pragma unroll
+    for (int mt = 0; mt < MTI; ++mt)
+      xp[mt] = act + static_cast<size_t>(c.row0 + min(16 * mt + r, c.nrows - 1)) * rowq + g + kc * 4;
     const uint4* wrun = uniform_ptr(wd + (static_cast<size_t>(c.e) * ntiles + ht0) * KC * kWave);
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
         wv[u][nb] = load_weight<kPolicyPlain>(wrun, NB * KC * kWave * 16, (nb * KC + kc + u) * kWave + lane);
-      xv[u] = xp[u * 4];
+#pragma unroll
+      for (int mt = 0; mt < MTI; ++mt) xv[u][mt] = xp[mt][u * 4];
     }
   };
-  floatx4 acc[NB];
+  floatx4 acc[NB][MTI];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](uint4 (&wv)[kU][NB], uint4 (&xv)[kU], Cursor& c) {
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int mt = 0; mt < MTI; ++mt) acc[nb][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](uint4 (&wv)[kU][NB], uint4 (&xv)[kU][MTI], Cursor& c) {
 #pragma unroll
     for (int u = 0; u < kU; ++u)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[nb] = P::mma(xv[u], wv[u][nb], acc[nb]);
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int mt = 0; mt < MTI; ++mt) acc[nb][mt] = P::mma(xv[u][mt], wv[u][nb], acc[nb][mt]);
     if (c.q == L - 1) {
-      // item done: out_w[t] += gate * row, rows 4g..4g+3 of the block, column r of each tile
+      // item done: out_w[t] += gate * row, rows 16 mt + 4g .. +3 of the item, column r of each tile
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = 4 * g + i;
-        if (m < c.nrows) {
-          const int row = c.row0 + m;
-          float* dst = accw + sh.tok[row] * kCols + r;
-          const float gt = sh.gw[row];
+      for (int mt = 0; mt < MTI; ++mt) {
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) dst[16 * nb] += gt * acc[nb][i];
+        for (int i = 0; i < 4; ++i) {
+          const int m = 16 * mt + 4 * g + i;
+          if (m < c.nrows) {
+            const int row = c.row0 + m;
+            float* dst = accw + sh.tok[row] * kCols + r;
+            const float gt = sh.gw[row];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) dst[16 * nb] += gt * acc[nb][mt][i];
+          }
         }
       }
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int mt = 0; mt < MTI; ++mt) acc[nb][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
     advance(c);
   };
@@ -1120,19 +1140,28 @@ hipError_t launch_down_rows(const ForwardParams& p, int cap, hipStream_t stream)
 // (one GPU's share of a tensor-parallel split) give lengths like 3, where
 // 3-step stages ran 11 % faster than single steps.
 struct ColShape {
-  int ksplit, ku, nb;
+  int ksplit, ku, nb, mti;
 };
 
-ColShape col_shape(int H, int I, int is_bf16) {
+#ifndef AMOE_COL_MTI
+#define AMOE_COL_MTI 0
+#endif
+
+// M-tiles per down item: two (items of up to 32 tokens) for blocks of more
+// than 32 tokens, where experts typically receive more than 16 tokens; with
+// two M-tiles the stages are capped at 6 k-steps (one column tile) or 4 (two).
+ColShape col_shape(int T, int H, int I, int is_bf16) {
   const int KC = I / (is_bf16 ? Bf16Path::kKF : F32Path::kKF);
   const int ntiles = H / 16;
   ColShape c;
   c.nb = (ntiles >= 256 && ntiles % 2 == 0) ? 2 : 1;
+  c.mti = AMOE_COL_MTI ? AMOE_COL_MTI : (T > 32 ? 2 : 1);
   c.ksplit = (ntiles / c.nb <= 128 && KC % 2 == 0) ? 2 : 1;
   const int len = KC / c.ksplit;
+  const int ku_max = c.nb == 1 ? (c.mti == 1 ? 12 : 6) : 4;
   c.ku = 1;
   for (const int u : {12, 8, 6, 4, 3, 2}) {
-    if (len % u == 0 && u <= (c.nb == 1 ? 12 : 4)) {
+    if (len % u == 0 && u <= ku_max) {
       c.ku = u;
       break;
     }
@@ -1147,28 +1176,35 @@ bool use_col_path(int T, int k) {
          static_cast<long long>(T) * k <= kSelfMaxSlots;
 }
 
-template <class P, int NB>
+template <class P, int NB, int MTI>
 hipError_t launch_down_col_nb(const ForwardParams& p, const ColShape& c, hipStream_t stream) {
   const dim3 grid((p.H / 16 / NB) * c.ksplit);
   constexpr int threads = kColLanes / NB * kWave;
   if constexpr (NB == 1) {  // deeper stages only with one column tile (col_shape)
-    if (c.ku == 12 || c.ku == 8 || c.ku == 6) {
-      if (c.ku == 12) down_col_kernel<P, 12, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
-      else if (c.ku == 8) down_col_kernel<P, 8, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
-      else down_col_kernel<P, 6, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+    if constexpr (MTI == 1) {
+      if (c.ku == 12 || c.ku == 8) {
+        if (c.ku == 12) down_col_kernel<P, 12, NB, MTI><<<grid, threads, 0, stream>>>(p, c.ksplit);
+        else down_col_kernel<P, 8, NB, MTI><<<grid, threads, 0, stream>>>(p, c.ksplit);
+        return hipGetLastError();
+      }
+    }
+    if (c.ku == 6) {
+      down_col_kernel<P, 6, NB, MTI><<<grid, threads, 0, stream>>>(p, c.ksplit);
       return hipGetLastError();
     }
   }
-  if (c.ku == 4) down_col_kernel<P, 4, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
-  else if (c.ku == 3) down_col_kernel<P, 3, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
-  else if (c.ku == 2) down_col_kernel<P, 2, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
-  else down_col_kernel<P, 1, NB><<<grid, threads, 0, stream>>>(p, c.ksplit);
+  if (c.ku == 4) down_col_kernel<P, 4, NB, MTI><<<grid, threads, 0, stream>>>(p, c.ksplit);
+  else if (c.ku == 3) down_col_kernel<P, 3, NB, MTI><<<grid, threads, 0, stream>>>(p, c.ksplit);
+  else if (c.ku == 2) down_col_kernel<P, 2, NB, MTI><<<grid, threads, 0, stream>>>(p, c.ksplit);
+  else down_col_kernel<P, 1, NB, MTI><<<grid, threads, 0, stream>>>(p, c.ksplit);
   return hipGetLastError();
 }
 
 template <class P>
 hipError_t launch_down_col(const ForwardParams& p, const ColShape& c, hipStream_t stream) {
-  return c.nb == 2 ? launch_down_col_nb<P, 2>(p, c, stream) : launch_down_col_nb<P, 1>(p, c, stream);
+  if (c.mti == 2)
+    return c.nb == 2 ? launch_down_col_nb<P, 2, 2>(p, c, stream) : launch_down_col_nb<P, 1, 2>(p, c, stream);
+  return c.nb == 2 ? launch_down_col_nb<P, 2, 1>(p, c, stream) : launch_down_col_nb<P, 1, 1>(p, c, stream);
 }
 
 }  // namespace
@@ -1240,8 +1276,9 @@ void forward_carve(void* ws, ForwardParams& p) {
 
 hipError_t launch_forward(ForwardParams p, hipStream_t stream) {
   const bool col = use_col_path(p.T, p.k);
-  const ColShape cs = col_shape(p.H, p.I, p.is_bf16);
+  const ColShape cs = col_shape(p.T, p.H, p.I, p.is_bf16);
   p.zero_out = col && cs.ksplit == 2;
+  p.item_rows = 16 * cs.mti;
   const bool small_k = p.k <= 8;
   hipError_t err = hipSuccess;
   if (!col) {

@@ -86,6 +86,7 @@ struct ForwardParams {
   int32_t* n_items;   // [1]
   int T, H, I, E, k, is_bf16;
   int zero_out;       // gate/up pass clears out (the down pass then adds two halves into it)
+  int item_rows;      // tokens per column-tile down item (16 per M-tile)
 };
 
 size_t forward_workspace_bytes(int T, int H, int I, int E, int k, int is_bf16);
