@@ -76,6 +76,12 @@ def parse():
     ap.add_argument("--tp-share", type=int, default=1, metavar="G",
                     help="time one GPU's share of a G-way tensor-parallel split over I: the same routing "
                          "(router, hidden states and trees as the full layer), experts with I/G rows")
+    ap.add_argument("--ceiling", action="store_true",
+                    help="reference rates of this GPU: read-only and copy streaming with plain torch kernels, "
+                         "and the cost of an empty launch inside a HIP graph")
+    ap.add_argument("--sweep-experts", default="",
+                    help="comma-separated routed-expert counts n: forward time at --config with exactly n "
+                         "experts routed (tokens spread evenly), e.g. 12,16,17,...")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="only run a plain device copy of MB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -385,6 +391,12 @@ def main():
         return
     if args.estimate:
         estimate_report(args)
+        return
+    if args.ceiling:
+        ceiling_report(args)
+        return
+    if args.sweep_experts:
+        sweep_experts_report(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the layer runs on a single MI355X; "
@@ -836,6 +848,120 @@ def estimate_report(args):
         log(f"{name}: |S'| estimated {sh['estimated']['S_prime']['mean']} synthetic {sh['synthetic']['S_prime']['mean']}")
     report["data"] = "synthetic"
     print(json.dumps(report), flush=True)
+
+
+def ceiling_report(args):
+    """Reference rates of the GPU the bench runs on, with plain torch kernels
+    (not this library's): a read-only reduction and a device copy over 4 GiB
+    buffers (bytes moved / time), and an empty launch inside a HIP graph (a
+    one-element fill, 200 launches per graph)."""
+    import torch
+
+    dev = "cuda"
+    res = {"report": "streaming and launch reference rates (plain torch kernels)"}
+    n = 2 << 30                                   # 2 Gi bf16 elements = 4 GiB
+    a = torch.ones(n, dtype=torch.bfloat16, device=dev)
+    b = torch.empty_like(a)
+    acc = torch.zeros((), dtype=torch.float32, device=dev)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / reps
+
+    t_read = timed(lambda: acc.copy_(a.sum(dtype=torch.float32)), 10)
+    t_copy = timed(lambda: b.copy_(a), 10)
+    res["read_GBs"] = round(2 * n / t_read / 1e9, 1)
+    res["copy_GBs"] = round(2 * 2 * n / t_copy / 1e9, 1)
+    del a, b
+    tiny = torch.zeros(1, dtype=torch.float32, device=dev)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        tiny.fill_(1.0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for _ in range(200):
+                tiny.fill_(1.0)
+    g.replay()
+    torch.cuda.synchronize()
+    t_g = timed(g.replay, 20)
+    res["graph_launch_us"] = round(t_g / 200 * 1e6, 2)
+    res["bytes"] = {"read": 2 * n, "copy_read_plus_write": 4 * n}
+    print(json.dumps(res), flush=True)
+
+
+def sweep_experts_report(args):
+    """Forward time against the exact number of routed experts n at one block
+    shape: T tokens with k slots each, slot j of token t routed to expert
+    (t k + j) mod n of a random n-subset (every token k distinct experts, the
+    tokens spread evenly over the n experts); 4 weight sets rotate; each n
+    timed as graph replays of the forward launches."""
+    import torch
+
+    from paper_2608_02989_amd import ops
+    from paper_2608_02989_amd import workload as W
+
+    dev = "cuda"
+    cfg = W.CONFIGS[args.config]
+    T, k, E = cfg.total_tokens, cfg.k, cfg.E
+    sets = 4
+    wl = []
+    for s_ in range(sets):
+        wg, wu, wd = W.expert_weights_torch(cfg, s_, dev)
+        wl.append((ops.pack_gate_up_weights(wg, wu), ops.pack_expert_weights(wd)))
+        del wg, wu, wd
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    rng = np.random.default_rng(0)
+    hb = W.bf16_round(rng.standard_normal((T, cfg.H)).astype(np.float32)).view(np.int16)
+    h = torch.from_numpy(hb).view(torch.bfloat16).to(dev)
+    out = torch.empty((T, cfg.H), dtype=torch.float32, device=dev)
+    ws = ops.forward_workspace(T, cfg.H, cfg.I, E, k, torch.bfloat16, dev)
+    gate = torch.full((T, k), 1.0 / k, dtype=torch.float32, device=dev)
+    stream = torch.cuda.Stream()
+    rows = []
+    for n in [int(x) for x in args.sweep_experts.split(",")]:
+        if n < k or n > E:
+            raise SystemExit(f"--sweep-experts: n must be in [k, E] = [{k}, {E}] (got {n})")
+        routs = []
+        for s_ in range(sets):
+            ex = rng.permutation(E)[:n]
+            idx = np.array([[ex[(t * k + j) % n] for j in range(k)] for t in range(T)], np.int32)
+            routs.append(torch.from_numpy(idx).to(dev))
+
+        def run():
+            for s_ in range(sets):
+                ops.moe_forward(h, wl[s_][0], wl[s_][1], routs[s_], gate, out=out, workspace=ws, stream=stream)
+        with torch.cuda.stream(stream):
+            run()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(stream):
+            with torch.cuda.graph(g, stream=stream):
+                run()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        with torch.cuda.stream(stream):
+            for _ in range(10):
+                g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / (10 * sets)
+        mb = n * cfg.expert_bytes / 1e6
+        rows.append({"n": n, "forward_us": round(us, 2), "weight_MB": round(mb, 1), "TBs": round(mb / us, 3)})
+        print(f"n={n} {us:.1f} us {mb / us:.2f} TB/s", file=sys.stderr, flush=True)
+        del g
+    print(json.dumps({"report": "forward time vs routed experts", "config": cfg.name, "T": T, "k": k,
+                      "rows": rows}), flush=True)
 
 
 def modes_report(args):
