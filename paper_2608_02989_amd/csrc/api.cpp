@@ -127,6 +127,8 @@ int32_t acceptmoe_route(const void* hidden, int32_t hidden_dtype, const void* ro
   if (hidden_dtype != ACCEPTMOE_F32 && hidden_dtype != ACCEPTMOE_BF16)
     return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: unknown hidden dtype %d", hidden_dtype);
   if (T == 0) return ACCEPTMOE_OK;
+  if ((T + 15) / 16 > 65535)
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "route: T must be <= %d (got %d)", 65535 * 16, T);
   if (!hidden || !router_packed || !logits) return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: null pointer");
   if (!aligned(hidden, 16) || !aligned(router_packed, 16) || !aligned(logits, 4))
     return fail(ACCEPTMOE_ERR_INVALID_ARG, "route: hidden/router_packed must be 16-byte aligned");
@@ -249,6 +251,8 @@ int32_t acceptmoe_moe_forward(const void* hidden, int32_t dtype, const void* w_g
   if (T == 0) return ACCEPTMOE_OK;
   if (static_cast<long long>(T) * k > (1ll << 30))
     return fail(ACCEPTMOE_ERR_UNSUPPORTED, "forward: T*k too large");
+  if (static_cast<long long>((H / 4 + 255) / 256) * T >= (1ll << 31))
+    return fail(ACCEPTMOE_ERR_UNSUPPORTED, "forward: T * ceil(H / 1024) must stay below 2^31 (T=%d H=%d)", T, H);
   if (!hidden || !w_gate_up || !w_down || !topk_idx || !topk_gate || !out)
     return fail(ACCEPTMOE_ERR_INVALID_ARG, "forward: null pointer");
   if (!aligned(hidden, 16) || !aligned(w_gate_up, 16) || !aligned(w_down, 16) || !aligned(out, 16))

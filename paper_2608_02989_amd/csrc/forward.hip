@@ -1057,12 +1057,14 @@ __global__ __launch_bounds__(kColLanes / NB * kWave) void down_col_kernel(Forwar
 // ---------------------------------------------------------------------------
 // combine: out[t, h] = sum over the dispatched slots of token t, in slot order.
 // The routing row and all k expert rows are loaded before any is used (rows
-// of skipped slots are read but discarded).
+// of skipped slots are read but discarded).  Workgroup b covers token
+// b / hblocks, float4 columns 256 (b % hblocks) ..; a one-dimensional grid, so
+// any T fits.
 // ---------------------------------------------------------------------------
 template <int KMAX>
-__global__ __launch_bounds__(256) void combine_kernel(ForwardParams p) {
-  const int t = blockIdx.y;
-  const int h4 = blockIdx.x * blockDim.x + threadIdx.x;  // float4 column
+__global__ __launch_bounds__(256) void combine_kernel(ForwardParams p, int hblocks) {
+  const int t = blockIdx.x / hblocks;
+  const int h4 = (blockIdx.x % hblocks) * blockDim.x + threadIdx.x;  // float4 column
   const int H = p.H, k = p.k;
   if (h4 * 4 >= H) return;
   int ev[KMAX];
@@ -1303,11 +1305,12 @@ hipError_t launch_forward(ForwardParams p, hipStream_t stream) {
   else
     err = small_t ? launch_down_rows<F32Path, 2>(p, cap, stream) : launch_down_rows<F32Path, 4>(p, cap, stream);
   if (err != hipSuccess) return err;
-  dim3 cgrid((p.H / 4 + 255) / 256, p.T);
+  const int hblocks = (p.H / 4 + 255) / 256;
+  const dim3 cgrid(static_cast<unsigned>(hblocks) * static_cast<unsigned>(p.T));
   if (small_k)
-    combine_kernel<8><<<cgrid, 256, 0, stream>>>(p);
+    combine_kernel<8><<<cgrid, 256, 0, stream>>>(p, hblocks);
   else
-    combine_kernel<kMaxTopK><<<cgrid, 256, 0, stream>>>(p);
+    combine_kernel<kMaxTopK><<<cgrid, 256, 0, stream>>>(p, hblocks);
   return hipGetLastError();
 }
 

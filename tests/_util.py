@@ -20,11 +20,12 @@ GATE_RTOL = 1.2e-7        # gates: fp64 on both sides, one fp32 rounding each (<
 # Per-row bound: max_h |y_th - yref_th| / max_h |yref_th| for every output row t
 # (a row is one token's layer output).  bf16: the SwiGLU activation is stored
 # in bf16 before the down projection, each element rounded with relative error
-# <= u = 2^-9; summed over I terms of random sign that error stays ~u of a
-# row's largest output (measured 1.0-1.5 u at every workload shape), so 3u
-# bounds it.  fp32: accumulation over H or I <= 4096 terms, ~sqrt(H) 2^-24 of
-# the row (measured <= 6e-7); 1e-5 bounds it.
-ROW_TOL = {"f32": 1e-5, "bf16": 3 * 2.0 ** -9}
+# <= u = 2^-9; summed over I terms of random sign that error stays near u of a
+# row's largest output (measured 1.0-1.5 u at every workload shape, 2.5 u as
+# the worst of 65,600 rows with only I = 32 terms); 1e-2 (~5 u) bounds it.
+# fp32: accumulation over H or I <= 4096 terms, ~sqrt(H) 2^-24 of the row
+# (measured <= 6e-7); 1e-5 bounds it.
+ROW_TOL = {"f32": 1e-5, "bf16": 1e-2}
 
 
 def normwise_rel(got, ref) -> float:

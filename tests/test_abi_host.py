@@ -79,6 +79,7 @@ def test_route_rejects():
     f = L.lib().acceptmoe_route
     assert status_and_msg(f(FAKE, L.BF16, FAKE, -1, 256, 16, FAKE, None))[0] == L.ERR_INVALID_ARG
     assert f(FAKE, L.BF16, FAKE, 8, 256, 0, FAKE, None) == L.ERR_UNSUPPORTED
+    assert f(FAKE, L.BF16, FAKE, 65535 * 16 + 1, 256, 16, FAKE, None) == L.ERR_UNSUPPORTED   # token tiles
     assert f(FAKE, L.BF16, FAKE, 8, 256, 513, FAKE, None) == L.ERR_UNSUPPORTED
     assert f(FAKE, L.BF16, FAKE, 8, 250, 16, FAKE, None) == L.ERR_UNSUPPORTED
     assert f(FAKE, 7, FAKE, 8, 256, 16, FAKE, None) == L.ERR_INVALID_ARG
@@ -219,3 +220,6 @@ def test_forward_rejects():
     assert fwd(h=V(0x100008)) == L.ERR_INVALID_ARG         # misaligned
     assert fwd() == L.ERR_WORKSPACE
     assert fwd(T=0, h=None, out=None) == L.OK
+    # the combine grid holds T * ceil(H / 1024) workgroups in one dimension
+    rc, msg = status_and_msg(fwd(T=1 << 24, H=512 * 1024, k=1))
+    assert rc == L.ERR_UNSUPPORTED and "2^31" in msg, msg

@@ -377,6 +377,22 @@ def test_forward_no_routed_expert(gpu, T):
     check_forward(out.cpu().numpy(), ref, cfg.dtype, f"routed after unrouted T={T}")
 
 
+# more tokens than a grid's y dimension holds (65,535): the per-slot path and its
+# combine over 65,600 tokens of a small layer
+def test_forward_parity_many_tokens(gpu):
+    T = 65_600
+    cfg = W.LayerConfig("many", 99, "bf16", T=T, B=1, H=64, E=6, k=2, I=32, depth_max=6,
+                        commit_rule="depth_sibling", hidden_std=1.0)
+    rng = np.random.default_rng(65_600)
+    h32 = rng.standard_normal((T, cfg.H)).astype(np.float32)
+    idx = np.stack([rng.permutation(cfg.E)[:cfg.k] for _ in range(T)]).astype(np.int32)
+    gate = rng.random((T, cfg.k)).astype(np.float32)
+    say(f"forward many tokens T={T}")
+    got, h64, (wg, wu, wd) = forward_case(cfg, idx, gate, h32)
+    ref = O.moe_forward_grouped(h64, wg, wu, wd, idx, gate, cfg.dtype)
+    check_forward(got, ref, cfg.dtype, f"many tokens T={T}")
+
+
 # forward path limits: k > 8 in the in-LDS dispatch, exactly 256 tokens / 2048
 # slots (largest column-tile block), 257 tokens (per-slot pass), E = 48
 @pytest.mark.parametrize("T,k,E,dtype", [(40, 32, 64, "bf16"), (37, 12, 48, "f32"), (256, 8, 64, "bf16"),
