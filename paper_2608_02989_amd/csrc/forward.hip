@@ -371,12 +371,16 @@ __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f +
 
 // Weight streams.  Every weight fragment is read once per step, through a
 // buffer load whose cache policy is chosen per pass: the gate/up stream is
-// non-temporal, the down stream uses the default policy.  (Measured on the
-// wide layer, H = 4096, I = 1536: the column-tile down pass takes 68.6 us
-// with default-policy loads against 75.6 us non-temporal, the per-slot down
-// pass at 512 tokens 375 against 396 us; the gate/up pass is fastest
-// non-temporal, 601 against 612 us for plain global non-temporal loads and
-// 621 us with the default policy.)  A weight run is addressed by a
+// non-temporal; the down stream uses the default policy where H >= 4096 (two
+// column tiles per workgroup, or the per-slot pass) and is non-temporal
+// otherwise.  (Measured on the wide layer, H = 4096, I = 1536: the column-tile
+// down pass takes 68.6 us with default-policy loads against 75.6 us
+// non-temporal, the per-slot down pass at 512 tokens 375 against 396 us; the
+// gate/up pass is fastest non-temporal, 601 against 612 us for plain global
+// non-temporal loads and 621 us with the default policy.  At H = 2048 the
+// default policy saves 0.8 us of the down pass but lets its weights evict the
+// next layer's router planes from the Infinity Cache: the 48-layer pass ran
+// 5027 against 4941 us per block.)  A weight run is addressed by a
 // wave-uniform base and its length in bytes: a load past the run returns
 // zero instead of reading other memory.
 constexpr int kPolicyStream = 2;  // "nt": non-temporal
@@ -980,7 +984,8 @@ __global__ __launch_bounds__(kColLanes / NB * kWave) void down_col_kernel(Forwar
     for (int u = 0; u < kU; ++u) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
-        wv[u][nb] = load_weight<kPolicyPlain>(wrun, NB * KC * kWave * 16, (nb * KC + kc + u) * kWave + lane);
+        wv[u][nb] = load_weight<NB == 2 ? kPolicyPlain : kPolicyStream>(wrun, NB * KC * kWave * 16,
+                                                                        (nb * KC + kc + u) * kWave + lane);
 #pragma unroll
       for (int mt = 0; mt < MTI; ++mt) xv[u][mt] = xp[mt][u * 4];
     }
@@ -1150,14 +1155,17 @@ struct ColShape {
 #endif
 
 // M-tiles per down item: two (items of up to 32 tokens) for blocks of more
-// than 32 tokens, where experts typically receive more than 16 tokens; with
-// two M-tiles the stages are capped at 6 k-steps (one column tile) or 4 (two).
+// than 32 tokens when the workgroup owns two column tiles, whose stages are
+// capped at 4 k-steps either way (H = 4096, T = 64: forward 188.7 -> 182.9 us);
+// with one column tile a second M-tile would halve the 12-k-step stages, which
+// cost more than it saves where experts receive ~10 tokens (H = 2048, T = 60:
+// 48-layer pass 4926 -> 5063 us per block).
 ColShape col_shape(int T, int H, int I, int is_bf16) {
   const int KC = I / (is_bf16 ? Bf16Path::kKF : F32Path::kKF);
   const int ntiles = H / 16;
   ColShape c;
   c.nb = (ntiles >= 256 && ntiles % 2 == 0) ? 2 : 1;
-  c.mti = AMOE_COL_MTI ? AMOE_COL_MTI : (T > 32 ? 2 : 1);
+  c.mti = AMOE_COL_MTI ? AMOE_COL_MTI : (T > 32 && c.nb == 2 ? 2 : 1);
   c.ksplit = (ntiles / c.nb <= 128 && KC % 2 == 0) ? 2 : 1;
   const int len = KC / c.ksplit;
   const int ku_max = c.nb == 1 ? (c.mti == 1 ? 12 : 6) : 4;
