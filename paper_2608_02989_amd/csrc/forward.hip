@@ -771,13 +771,17 @@ union SelfDispatchSlot<false, KMAX> {
 // Work item i = (active expert i / wg_per_expert, tile run i % wg_per_expert).
 // Without kSelf: grid.x = cap_experts * wg_per_expert, one item per
 // workgroup, reading dispatch_kernel's CSR.  kSelf (gate/up pass, blocks of up
-// to kSelfMaxT tokens): a grid no larger than what is resident at once (so no
-// workgroup waits for a slot) takes items blockIdx.x, blockIdx.x + gridDim.x,
-// ..., each with its own per-item dispatch; the last workgroup, which has the
-// fewest items, builds the full CSR afterwards and publishes it for the down
-// pass.  (A device-wide work counter was tried: every workgroup's first atomic
-// hits the same address at once and the serialized atomics cost more than
-// the balance gained.)
+// to kSelfMaxT tokens): a grid of up to kSelfGridMult times the workgroups
+// resident at once takes items blockIdx.x, blockIdx.x + gridDim.x, ..., each
+// with its own per-item dispatch.  The workgroups beyond the resident ones
+// start on whichever CU frees a slot first, which evens out the CUs' finish
+// times (CUs stream at up to 20 % different rates): at H = 4096, T = 64 the
+// pass took 121.1 us with a resident-sized grid and 117.8 us with three times
+// that; workgroups left without an item exit after the prologue.  Workgroup
+// 0, which is dispatched first and has the most items, builds the full CSR
+// afterwards and publishes it for the down pass.  (Claiming items from a
+// device-wide counter was measured no better.)
+constexpr int kSelfGridMult = 3;
 
 // Occupancy floor: three workgroups per CU for up to two M-tiles, two for
 // more (the register budget the streaming loop is tuned to).
@@ -870,7 +874,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MTMAX <= 2 
       run_expert((item % wg_per_expert) * tpw, e, __builtin_amdgcn_readfirstlane(n_e),
                  __builtin_amdgcn_readfirstlane(o_e), id.ent);
     }
-    if (blockIdx.x == gridDim.x - 1) {
+    if (blockIdx.x == 0) {
       __syncthreads();  // the per-item state shares this LDS
       SelfDispatch& sd = sds.sd;
       self_dispatch<KMAX>(p, sd, tid);
@@ -1118,11 +1122,11 @@ hipError_t launch_gate_up(const ForwardParams& p, int cap, bool self, hipStream_
     ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, false, 8><<<dim3(items), 256, 0, stream>>>(p);
   } else if (p.k <= 8) {
     auto kern = ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, 8>;
-    const int res = resident_workgroups(kern);
+    const int res = kSelfGridMult * resident_workgroups(kern);
     kern<<<dim3(items < res ? items : res), 256, 0, stream>>>(p);
   } else {
     auto kern = ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, kMaxTopK>;
-    const int res = resident_workgroups(kern);
+    const int res = kSelfGridMult * resident_workgroups(kern);
     kern<<<dim3(items < res ? items : res), 256, 0, stream>>>(p);
   }
   return hipGetLastError();
