@@ -16,6 +16,8 @@
 //
 // Weights are read in the packed fragment layout (see
 // acceptmoe_pack_expert_weights): one wave load = one contiguous 1 KiB block.
+#include <type_traits>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -639,15 +641,19 @@ struct ProjShape {
 };
 
 // ent_e: the n_e slot ids of expert e in node order; o_e: its first row in act
-template <class P, Proj F, int MT, int NTW, int KS>
+template <class P, Proj F, int MT, int NTW, int KS, int MG>
 __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* ent_e, int e, int tile_base, int n_e,
                                          int o_e, int m0, floatx4 (*red)[kWave][4], uint4* xs) {
   static_assert(F != Proj::GateUp || NTW == 2, "the packed gate/up layout holds tile pairs");
+  static_assert(KS % MG == 0, "M groups take waves from the K split");
   constexpr int NB = ProjShape<F, NTW, KS>::kNB;
+  constexpr int KSe = KS / MG;  // waves per K split of one (tile group, M group)
+  constexpr int TG = 4 / KS;    // tile groups per workgroup
   const int wave = wave_id(), lane = lane_id();
   const int r = lane & 15, g = lane >> 4;
-  const int sub = wave % KS;
-  const int tile0 = tile_base + (wave / KS) * NTW;  // first of this wave's NTW tiles
+  const int sub = wave % KSe;
+  const int tile0 = tile_base + ((wave / KSe) % TG) * NTW;  // first of this wave's NTW tiles
+  m0 += (wave / (KSe * TG)) * MT * 16;                      // this wave's M group
   const int ntiles = (F == Proj::GateUp ? p.I : p.H) / 16;
   const int K = F == Proj::GateUp ? p.H : p.I;
   const int KC = K / P::kKF;
@@ -701,12 +707,12 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* 
   for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[nb][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  if constexpr (KS == 1)
+  if constexpr (KS == 1 && MG == 1)
     stream_tiles_shared<P, MT, NB, kPolicy>(w, wbytes, x, KC, wstride, acc, xs);
   else
-    stream_tiles<P, MT, NB, kPolicy>(w, wbytes, x, sub, KS, (KC - sub + KS - 1) / KS, wstride, acc);
+    stream_tiles<P, MT, NB, kPolicy>(w, wbytes, x, sub, KSe, (KC - sub + KSe - 1) / KSe, wstride, acc);
 
-  if constexpr (KS > 1) {
+  if constexpr (KSe > 1) {
     // fixed-order sum of the KS partial tiles, four fragments per LDS round
 #pragma unroll
     for (int q0 = 0; q0 < NB * MT; q0 += 4) {
@@ -716,7 +722,7 @@ __device__ __forceinline__ void ffn_pass(const ForwardParams& p, const int32_t* 
       __syncthreads();
       if (sub == 0) {
 #pragma unroll
-        for (int s2 = 1; s2 < KS; ++s2)
+        for (int s2 = 1; s2 < KSe; ++s2)
 #pragma unroll
           for (int q = 0; q < 4; ++q)
             if (q0 + q < NB * MT) {
@@ -802,13 +808,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MTMAX <= 2 
          i += static_cast<size_t>(gridDim.x) * blockDim.x)
       o4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
+  // An expert with more than MTMAX M-tiles of tokens would stream its weights
+  // once per MTMAX M-tiles.  Without the in-workgroup dispatch (blocks of more
+  // than kSelfMaxT tokens) such an expert instead takes the waves of the K
+  // split as M groups: MG = 2 or 4 groups of MT M-tiles each read the same
+  // weight fragments (from L1 or L2 after the first), so the weights come
+  // from HBM once per up to 4 MTMAX M-tiles.  At 512 tokens (8 trees of 64,
+  // H = 4096) experts receive up to ~160 tokens and the forward took 1014.5
+  // us with one pass per MTMAX M-tiles, 972.3 us with M groups.  Every wave
+  // of the workgroup runs the same instantiation (the passes hold barriers).
+  auto pass_mt = [&](auto mg_tag, int mt, int tile_base, int e, int n_e, int o_e, int m0, const int32_t* ent_e) {
+    constexpr int G = decltype(mg_tag)::value;
+    if (mt == 1) ffn_pass<P, F, 1, NTW, KS, G>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
+    else if (MTMAX >= 2 && mt == 2) ffn_pass<P, F, (MTMAX >= 2 ? 2 : 1), NTW, KS, G>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
+    else if (MTMAX >= 3 && mt == 3) ffn_pass<P, F, (MTMAX >= 3 ? 3 : 1), NTW, KS, G>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
+    else ffn_pass<P, F, MTMAX, NTW, KS, G>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
+  };
   auto run_expert = [&](int tile_base, int e, int n_e, int o_e, const int32_t* ent_e) {
-    for (int m0 = 0; m0 < n_e; m0 += 16 * MTMAX) {
-      const int nmt = min(MTMAX, (n_e - m0 + 15) / 16);
-      if (nmt == 1) ffn_pass<P, F, 1, NTW, KS>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
-      else if (MTMAX >= 2 && nmt == 2) ffn_pass<P, F, (MTMAX >= 2 ? 2 : 1), NTW, KS>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
-      else if (MTMAX >= 3 && nmt == 3) ffn_pass<P, F, (MTMAX >= 3 ? 3 : 1), NTW, KS>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
-      else ffn_pass<P, F, MTMAX, NTW, KS>(p, ent_e, e, tile_base, n_e, o_e, m0, red, xs);
+    for (int m0 = 0; m0 < n_e;) {
+      const int left = (n_e - m0 + 15) / 16;  // M-tiles still to cover
+      if (kSelf || left <= MTMAX || KS % 2 != 0) {
+        const int mt = min(MTMAX, left);
+        pass_mt(std::integral_constant<int, 1>{}, mt, tile_base, e, n_e, o_e, m0, ent_e);
+        m0 += 16 * mt;
+      } else if (KS % 4 == 0 && left > 2 * MTMAX) {
+        const int mt = (min(left, 4 * MTMAX) + 3) / 4;
+        pass_mt(std::integral_constant<int, (KS % 4 == 0 ? 4 : 1)>{}, mt, tile_base, e, n_e, o_e, m0, ent_e);
+        m0 += 64 * mt;
+      } else {
+        const int mt = (min(left, 2 * MTMAX) + 1) / 2;
+        pass_mt(std::integral_constant<int, (KS % 2 == 0 ? 2 : 1)>{}, mt, tile_base, e, n_e, o_e, m0, ent_e);
+        m0 += 32 * mt;
+      }
     }
   };
   if constexpr (kSelf) {
