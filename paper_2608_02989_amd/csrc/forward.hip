@@ -152,6 +152,7 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParam
   __shared__ int s_active[kMaxExperts];
   __shared__ int s_nact;
   __shared__ uint32_t s_mask[kMaxExperts * (kDispatchChunk / 32)];
+  __shared__ int s_pre[kMaxExperts * (kDispatchChunk / 32)];  // nodes of e in the chunk's earlier words
   const int tid = threadIdx.x;
   const int E = p.E, k = p.k, T = p.T;
   constexpr int words = kDispatchChunk / 32;
@@ -196,23 +197,29 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(ForwardParam
         if (valid & (1u << j)) atomicOr(&s_mask[ev[j] * words + (tid >> 5)], 1u << (tid & 31));
     }
     __syncthreads();
+    // per expert, exclusive prefix of the word popcounts
+    for (int e = tid; e < E; e += kDispatchThreads) {
+      int c = 0;
+      for (int w = 0; w < words; ++w) {
+        s_pre[e * words + w] = c;
+        c += __popc(s_mask[e * words + w]);
+      }
+    }
+    __syncthreads();
     if (t < T) {
 #pragma unroll
       for (int j = 0; j < KMAX; ++j) {
         if (valid & (1u << j)) {
-          const uint32_t* m = s_mask + ev[j] * words;
-          int before = 0;
-          for (int w = 0; w < (tid >> 5); ++w) before += __popc(m[w]);
-          before += __popc(m[tid >> 5] & ((1u << (tid & 31)) - 1u));
+          const int i = ev[j] * words + (tid >> 5);
+          const int before = s_pre[i] + __popc(s_mask[i] & ((1u << (tid & 31)) - 1u));
           p.ent_slot[s_off[ev[j]] + s_run[ev[j]] + before] = t * k + j;
         }
       }
     }
     __syncthreads();
     for (int e = tid; e < E; e += kDispatchThreads) {
-      int c = 0;
-      for (int w = 0; w < words; ++w) c += __popc(s_mask[e * words + w]);
-      s_run[e] += c;
+      const int i = e * words + words - 1;
+      s_run[e] += s_pre[i] + __popc(s_mask[i]);
     }
     __syncthreads();
   }
