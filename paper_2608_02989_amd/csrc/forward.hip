@@ -785,15 +785,19 @@ union SelfDispatchSlot<false, KMAX> {
 // Without kSelf: grid.x = cap_experts * wg_per_expert, one item per
 // workgroup, reading dispatch_kernel's CSR.  kSelf (gate/up pass, blocks of up
 // to kSelfMaxT tokens): a grid of up to kSelfGridMult times the workgroups
-// resident at once takes items blockIdx.x, blockIdx.x + gridDim.x, ..., each
-// with its own per-item dispatch.  The workgroups beyond the resident ones
-// start on whichever CU frees a slot first, which evens out the CUs' finish
-// times (CUs stream at up to 20 % different rates): at H = 4096, T = 64 the
-// pass took 121.1 us with a resident-sized grid and 117.8 us with three times
-// that; workgroups left without an item exit after the prologue.  Workgroup
-// 0, which is dispatched first and has the most items, builds the full CSR
-// afterwards and publishes it for the down pass.  (Claiming items from a
-// device-wide counter was measured no better.)
+// resident at once (H >= 4096; once otherwise) takes items blockIdx.x,
+// blockIdx.x + gridDim.x, ..., each with its own per-item dispatch.  The
+// workgroups beyond the resident ones start on whichever CU frees a slot
+// first, which evens out the CUs' finish times (CUs stream at up to 20 %
+// different rates): at H = 4096, T = 64 the pass took 121.1 us with a
+// resident-sized grid and 117.8 us with three times that.  The shorter items
+// of H = 2048 (256 KiB) do not repay the prologue each extra workgroup
+// repeats: the 48-layer pass at T = 60 ran 4951, 4990 and 5054 us per block
+// with one, two and three times the resident grid.  Workgroups left without
+// an item exit after the prologue.  Workgroup 0, which is dispatched first
+// and has the most items, builds the full CSR afterwards and publishes it for
+// the down pass.  (Claiming items from a device-wide counter was measured no
+// better.)
 constexpr int kSelfGridMult = 3;
 
 // Occupancy floor: three workgroups per CU for up to two M-tiles, two for
@@ -1160,11 +1164,11 @@ hipError_t launch_gate_up(const ForwardParams& p, int cap, bool self, hipStream_
     ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, false, 8><<<dim3(items), 256, 0, stream>>>(p);
   } else if (p.k <= 8) {
     auto kern = ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, 8>;
-    const int res = kSelfGridMult * resident_workgroups(kern);
+    const int res = (p.H >= 4096 ? kSelfGridMult : 1) * resident_workgroups(kern);
     kern<<<dim3(items < res ? items : res), 256, 0, stream>>>(p);
   } else {
     auto kern = ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, kMaxTopK>;
-    const int res = kSelfGridMult * resident_workgroups(kern);
+    const int res = (p.H >= 4096 ? kSelfGridMult : 1) * resident_workgroups(kern);
     kern<<<dim3(items < res ? items : res), 256, 0, stream>>>(p);
   }
   return hipGetLastError();
