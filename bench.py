@@ -357,8 +357,40 @@ def workload_text(wl: Workload, rho) -> str:
     return txt
 
 
+def attainable_read_gbs(nbytes: int) -> float:
+    """The rate a plain stream of nbytes reaches on this GPU
+    (acceptmoe_stream_read, best of 256 and 512 workgroups, each launch on a
+    fresh window of an 8 GiB buffer so the Infinity Cache holds none of it)."""
+    import torch
+
+    from paper_2608_02989_amd import ops
+
+    nbytes -= nbytes % 256
+    big = max(8 << 30, 4 * nbytes)
+    buf = torch.empty(big // 4, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(512, dtype=torch.int32, device="cuda")
+    windows = big // nbytes
+    best = 0.0
+    for g in (256, 512):
+        for i in range(3):
+            ops.stream_read(buf[(i % windows) * nbytes // 4:], nbytes, sink, g)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 20
+        e0.record()
+        for i in range(reps):
+            ops.stream_read(buf[((i + 3) % windows) * nbytes // 4:], nbytes, sink, g)
+        e1.record()
+        torch.cuda.synchronize()
+        best = max(best, nbytes / (e0.elapsed_time(e1) * 1e-3 / reps) / 1e9)
+    del buf, sink
+    torch.cuda.empty_cache()
+    return best
+
+
 def roofline_block(wl: Workload, m) -> dict:
     ratio = measured_traffic(wl.cfg.name) if wl.tp_share == 1 else None
+    read = attainable_read_gbs(int(m["fwd_bytes"]))
     return {"bound": "hbm",
             "kernel": "acceptmoe_moe_forward (gate/up + down passes of the grouped SwiGLU FFN)",
             "achieved": round(m["fwd_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -369,7 +401,8 @@ def roofline_block(wl: Workload, m) -> dict:
             "launch_timing": m["fwd_timing"],
             "eager_launch_us": round(m["fwd_eager_us"], 2), "eager_launch_p50_us": m["fwd_eager_p50"],
             "eager_achieved": round(m["fwd_eager_gbs"], 1),
-            "mfma_util": round(m["flops"] / (m["fwd_us"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5)}
+            "mfma_util": round(m["flops"] / (m["fwd_us"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5),
+            "attainable_read_GBs": round(read, 1), "frac_of_attainable": round(m["fwd_gbs"] / read, 4)}
 
 
 def summary(wl: Workload, m, rho) -> dict:
@@ -851,14 +884,57 @@ def estimate_report(args):
 
 
 def ceiling_report(args):
-    """Reference rates of the GPU the bench runs on, with plain torch kernels
-    (not this library's): a read-only reduction and a device copy over 4 GiB
-    buffers (bytes moved / time), and an empty launch inside a HIP graph (a
+    """Reference rates of the GPU the bench runs on: the library's plain
+    streaming read (acceptmoe_stream_read: contiguous shares, 16-byte
+    non-temporal loads, no arithmetic) over the byte counts of the headline
+    forward and its passes, each window moved through a 16 GiB buffer so no
+    launch rereads what the previous one left in the Infinity Cache, best over
+    workgroup counts; plain torch kernels for a read-only reduction and a
+    device copy over 4 GiB buffers; and an empty launch inside a HIP graph (a
     one-element fill, 200 launches per graph)."""
     import torch
 
+    from paper_2608_02989_amd import ops
+
     dev = "cuda"
-    res = {"report": "streaming and launch reference rates (plain torch kernels)"}
+    res = {"report": "streaming and launch reference rates"}
+    big = 16 << 30
+    buf = torch.ones(big // 4, dtype=torch.int32, device=dev)
+    sink = torch.zeros(65536, dtype=torch.int32, device=dev)
+    sizes = {"wide_offload down pass (25.25 experts)": int(25.25 * 4096 * 1536 * 2),
+             "wide_offload gate/up pass (25.25 experts)": int(25.25 * 2 * 4096 * 1536 * 2),
+             "wide_offload forward (25.25 experts)": int(25.25 * 3 * 4096 * 1536 * 2),
+             "1 GiB": 1 << 30, "batched_8x64 forward (116.4 experts)": int(116.4 * 3 * 4096 * 1536 * 2)}
+    grids = [256, 512, 1024, 2048, 4096, 8192]
+    reads = {}
+    for name, nb in sizes.items():
+        nb -= nb % 256
+        windows = big // nb
+        rates = {}
+        for g in grids:
+            def run(i, nb=nb, g=g):
+                off = (i % windows) * nb
+                ops.stream_read(buf[off // 4:], nb, sink, g)
+            for i in range(3):
+                run(i)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            reps = 20
+            e0.record()
+            for i in range(reps):
+                run(i + 3)
+            e1.record()
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) * 1e-3 / reps
+            rates[g] = (round(t * 1e6, 2), round(nb / t / 1e9, 1))
+        best = max(rates, key=lambda g: rates[g][1])
+        reads[name] = {"bytes": nb, "best_grid": best, "us": rates[best][0], "GBs": rates[best][1],
+                       "by_grid_GBs": {g: v[1] for g, v in rates.items()}}
+        print(f"[ceiling] stream read {name}: {rates[best][1]} GB/s ({rates[best][0]} us, grid {best})",
+              file=sys.stderr, flush=True)
+    res["library_stream_read"] = reads
+    del buf, sink
+    torch.cuda.empty_cache()
     n = 2 << 30                                   # 2 Gi bf16 elements = 4 GiB
     a = torch.ones(n, dtype=torch.bfloat16, device=dev)
     b = torch.empty_like(a)
@@ -877,8 +953,8 @@ def ceiling_report(args):
 
     t_read = timed(lambda: acc.copy_(a.sum(dtype=torch.float32)), 10)
     t_copy = timed(lambda: b.copy_(a), 10)
-    res["read_GBs"] = round(2 * n / t_read / 1e9, 1)
-    res["copy_GBs"] = round(2 * 2 * n / t_copy / 1e9, 1)
+    res["torch_read_GBs"] = round(2 * n / t_read / 1e9, 1)
+    res["torch_copy_GBs"] = round(2 * 2 * n / t_copy / 1e9, 1)
     del a, b
     tiny = torch.zeros(1, dtype=torch.float32, device=dev)
     s = torch.cuda.Stream()

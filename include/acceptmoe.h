@@ -411,6 +411,18 @@ int32_t acceptmoe_pool_serve_wave(void* state, const int32_t* topk_idx, const in
 int32_t acceptmoe_copy_rows(const float* src, float* dst, const int32_t* row_tag, int32_t tag,
                             int32_t T, int32_t H, void* stream);
 
+/*
+ * acceptmoe_stream_read -- a measurement, not part of the method: reads the
+ * `bytes` bytes at src (device, 16-byte aligned, bytes % 16 == 0) with
+ * 16-byte non-temporal loads, `grid` workgroups of 256 threads each taking
+ * one contiguous share, and writes one XOR checksum word per workgroup to
+ * sink[0 .. grid) (device uint32).  Its time gives the HBM read rate a plain
+ * stream reaches on the device, the attainable counterpart of the expert-
+ * weight stream of acceptmoe_moe_forward.  1 <= grid <= 65535; bytes == 0 is
+ * a no-op.
+ */
+int32_t acceptmoe_stream_read(const void* src, size_t bytes, uint32_t* sink, int32_t grid, void* stream);
+
 /* Thread-local description of the last error (empty string if none). */
 const char* acceptmoe_last_error(void);
 

@@ -68,6 +68,7 @@ SIGNATURES = {
     "acceptmoe_pool_serve_wave": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _sz, _vp, _vp,
                                          _vp]),
     "acceptmoe_copy_rows": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _vp]),
+    "acceptmoe_stream_read": (_i32, [_vp, _sz, _vp, _i32, _vp]),
     "acceptmoe_last_error": (ctypes.c_char_p, []),
     "acceptmoe_version": (_i32, []),
 }

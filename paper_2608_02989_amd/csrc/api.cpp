@@ -296,4 +296,15 @@ int32_t acceptmoe_residual_add(const void* hidden, int32_t dtype, const float* y
   return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "residual_add launch");
 }
 
+int32_t acceptmoe_stream_read(const void* src, size_t bytes, uint32_t* sink, int32_t grid, void* stream) {
+  clear_err();
+  if (grid < 1 || grid > 65535) return fail(ACCEPTMOE_ERR_INVALID_ARG, "stream_read: grid must be in [1, 65535] (got %d)", grid);
+  if (bytes % 16 != 0) return fail(ACCEPTMOE_ERR_INVALID_ARG, "stream_read: bytes must be a multiple of 16 (got %zu)", bytes);
+  if (bytes == 0) return ACCEPTMOE_OK;
+  if (!src || !sink) return fail(ACCEPTMOE_ERR_INVALID_ARG, "stream_read: null pointer");
+  if (!aligned(src, 16) || !aligned(sink, 4)) return fail(ACCEPTMOE_ERR_INVALID_ARG, "stream_read: src must be 16-byte aligned");
+  hipError_t e = amoe::launch_stream_read(src, bytes, sink, grid, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ACCEPTMOE_OK : hip_fail(e, "stream_read launch");
+}
+
 }  // extern "C"

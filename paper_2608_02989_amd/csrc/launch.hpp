@@ -64,6 +64,7 @@ hipError_t launch_residual_add(const void* hidden, int is_bf16, const float* y, 
                                hipStream_t stream);
 hipError_t launch_copy_rows(const float* src, float* dst, const int32_t* row_tag, int tag, int T, int H,
                             hipStream_t stream);
+hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* sink, int grid, hipStream_t stream);
 hipError_t launch_pack_gate_up(const void* gate, const void* up, int is_bf16, int E, int I, int H, void* dst,
                                hipStream_t stream);
 

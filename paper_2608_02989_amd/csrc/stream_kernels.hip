@@ -1,6 +1,7 @@
 // Small stream kernels around the layer: the row copy that joins the outputs of
-// a block served in waves (expert offload) and the residual add that chains
-// stacked verify layers.
+// a block served in waves (expert offload), the residual add that chains
+// stacked verify layers, and a plain streaming read that measures the HBM
+// read rate the expert-weight stream is compared with.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -39,7 +40,42 @@ __global__ void copy_rows_kernel(const float4* __restrict__ src, float4* __restr
     dst[static_cast<size_t>(t) * H4 + c] = src[static_cast<size_t>(t) * H4 + c];
 }
 
+// XOR of the 16-byte pieces [b per, (b + 1) per) of src (clamped to n16) into
+// sink[b], for workgroup b: eight non-temporal loads in flight per thread
+// before any is used, the access pattern of a weight stream without the
+// arithmetic.  The XOR keeps every load live.
+__global__ __launch_bounds__(256) void stream_read_kernel(const uint4* __restrict__ src, size_t n16, size_t per,
+                                                         uint32_t* __restrict__ sink) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  constexpr int kU = 8;
+  const size_t base = blockIdx.x * per;
+  const size_t end = base + per < n16 ? base + per : n16;
+  uint32_t acc = 0u;
+  for (size_t i = base + threadIdx.x; i < end; i += 256 * kU) {
+    u32x4 v[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const size_t j = i + static_cast<size_t>(u) * 256;
+      v[u] = j < end ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + j)) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  __shared__ uint32_t part[4];
+  for (int o = 32; o >= 1; o >>= 1) acc ^= __shfl_xor(acc, o);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
+}
+
 }  // namespace
+
+hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* sink, int grid, hipStream_t stream) {
+  const size_t n16 = bytes / 16;
+  const size_t per = (n16 + grid - 1) / grid;
+  stream_read_kernel<<<grid, 256, 0, stream>>>(static_cast<const uint4*>(src), n16, per, sink);
+  return hipGetLastError();
+}
 
 hipError_t launch_copy_rows(const float* src, float* dst, const int32_t* row_tag, int tag, int T, int H,
                             hipStream_t stream) {

@@ -421,6 +421,17 @@ def copy_rows(src: torch.Tensor, dst: torch.Tensor, row_tag: torch.Tensor, tag: 
     check(lib().acceptmoe_copy_rows(_ptr(src), _ptr(dst), _ptr(row_tag), int(tag), T, H, _stream_ptr(stream)))
 
 
+def stream_read(src: torch.Tensor, nbytes: int, sink: torch.Tensor, grid: int, stream=None):
+    """Streams the first nbytes of the device tensor src with `grid`
+    workgroups, one checksum word each into sink (acceptmoe_stream_read; a
+    measurement of the attainable HBM read rate)."""
+    if not src.is_cuda or not sink.is_cuda or sink.dtype != torch.int32 or sink.numel() < grid:
+        raise ValueError("stream_read: src and an int32 sink of >= grid words on the GPU")
+    if nbytes > src.numel() * src.element_size():
+        raise ValueError("stream_read: nbytes exceeds src")
+    check(lib().acceptmoe_stream_read(_ptr(src), int(nbytes), _ptr(sink), int(grid), _stream_ptr(stream)))
+
+
 class OffloadLayer:
     """One MoE layer served from an X-slot pool (Sec. 3.4 offload paragraph).
 

@@ -223,3 +223,14 @@ def test_forward_rejects():
     # the combine grid holds T * ceil(H / 1024) workgroups in one dimension
     rc, msg = status_and_msg(fwd(T=1 << 24, H=512 * 1024, k=1))
     assert rc == L.ERR_UNSUPPORTED and "2^31" in msg, msg
+
+
+def test_stream_read_rejects():
+    f = L.lib().acceptmoe_stream_read
+    assert f(FAKE, 1024, FAKE, 0, None) == L.ERR_INVALID_ARG           # grid < 1
+    assert f(FAKE, 1024, FAKE, 65536, None) == L.ERR_INVALID_ARG       # grid > 65535
+    assert f(FAKE, 1000, FAKE, 4, None) == L.ERR_INVALID_ARG           # bytes % 16
+    assert f(None, 1024, FAKE, 4, None) == L.ERR_INVALID_ARG
+    assert f(FAKE, 1024, None, 4, None) == L.ERR_INVALID_ARG
+    assert f(V(0x100008), 1024, FAKE, 4, None) == L.ERR_INVALID_ARG    # misaligned
+    assert f(None, 0, None, 4, None) == L.OK                           # empty: no launch
