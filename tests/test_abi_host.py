@@ -234,3 +234,37 @@ def test_stream_read_rejects():
     assert f(FAKE, 1024, None, 4, None) == L.ERR_INVALID_ARG
     assert f(V(0x100008), 1024, FAKE, 4, None) == L.ERR_INVALID_ARG    # misaligned
     assert f(None, 0, None, 4, None) == L.OK                           # empty: no launch
+
+
+C_PROGRAM = r"""
+#include <stdio.h>
+#include "acceptmoe.h"
+int main(void) {
+  size_t ws = acceptmoe_select_workspace_size(64, 128, 8);
+  int32_t rc = acceptmoe_route(NULL, ACCEPTMOE_BF16, NULL, 64, 4096, 128, NULL, NULL);
+  printf("%d %zu %d\n", (int)acceptmoe_version(), ws, (int)rc);
+  return ws > 0 && rc == ACCEPTMOE_ERR_INVALID_ARG ? 0 : 1;
+}
+"""
+
+
+def test_header_is_c_and_links_from_c(tmp_path):
+    """The boundary is plain C: a C99 program including the header links
+    against the library and calls host-side entry points (no GPU work)."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("no gcc")
+    src = tmp_path / "abi.c"
+    src.write_text(C_PROGRAM)
+    exe = tmp_path / "abi"
+    libdir = os.path.dirname(L.LIB_PATH)
+    libname = os.path.basename(L.LIB_PATH)
+    assert libname.startswith("lib") and libname.endswith(".so")
+    cmd = ["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", "-I", os.path.join(ROOT, "include"),
+           str(src), "-o", str(exe), "-L", libdir, "-l" + libname[3:-3], "-Wl,-rpath," + libdir]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stdout + out.stderr
+    ver, ws, rc = out.stdout.split()
+    assert int(ver) == L.lib().acceptmoe_version() and int(ws) > 0 and int(rc) == L.ERR_INVALID_ARG
