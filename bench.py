@@ -9,13 +9,16 @@ weights through the 256 MB Infinity Cache.
 The headline workload is the largest single-tree configuration (H = 4096,
 I = 1536, T = 64 nodes, 25 % residency mask); the Qwen3-30B-A3B-shaped layer
 (T = 32) and the batched one (8 trees x 64 nodes) follow as companions, each
-with its own roofline block.  Prints one JSON line:
+with its own roofline block, each measured by this script in a child process
+(a fresh device allocator, as in a serving process).  Prints one JSON line:
   value      eligible-expert weight bytes streamed per second (GB/s) over the
              whole step (route + select + forward), bytes and time over the
              same timed steps
   roofline   the expert FFN launch (acceptmoe_moe_forward) against HBM peak,
              timed with HIP events around graph replays of the timed steps'
-             forward launches; traffic from committed rocprofv3 counters
+             forward launches; traffic from committed rocprofv3 counters;
+             the rate a plain stream of the same bytes reaches
+             (acceptmoe_stream_read) beside it
   cpu_baseline  the CPU oracle on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -414,6 +417,31 @@ def summary(wl: Workload, m, rho) -> dict:
             "natural_union": round(m["unat"], 2), "roofline": roofline_block(wl, m)}
 
 
+def companion_run(name: str, args, log) -> dict:
+    """One companion workload, measured by this script in a child process.
+    Each workload gets a fresh device allocator: after a large allocation was
+    freed in the same process, the Qwen3-30B-A3B forward measured 59.2 instead
+    of 56.8 us (a 20 GB allocate-and-free before it sufficed), so weights are
+    placed as a serving process would place them at start-up."""
+    import subprocess
+    cmd = [sys.executable, os.path.abspath(__file__), "--config", name, "--companions", "", "--no-alt",
+           "--cpu-seconds", "0", "--steps", str(args.steps), "--warmup", str(args.warmup), "--rho", str(args.rho),
+           "--graph", str(args.graph), "--blocks", str(args.blocks)]
+    out = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, check=True)
+    line = json.loads(out.stdout.strip().splitlines()[-1])
+    c = line["config"]
+    res = {"workload": c["workload"], "value": line["value"], "unit": line["unit"],
+           "latency_us": line["latency_us"], "eager_latency_us": line["eager_latency_us"],
+           "eager_step_p10_p50_p90_us": line["eager_step_p10_p50_p90_us"],
+           "weight_MB_per_step": c["weight_MB_per_step"], "routed_experts": c["routed_experts"],
+           "eligible": c["eligible"], "natural_union": c["natural_union"], "roofline": line["roofline"],
+           "timing": line["timing"]}
+    r = line["roofline"]
+    log(f"{name}: {line['latency_us']:.1f} us/step, {line['value']:.0f} GB/s, ffn {r['launch_us']:.1f} us "
+        f"({r['achieved']:.0f} GB/s), routed {c['routed_experts']:.1f} (child process)")
+    return res
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -474,12 +502,7 @@ def main():
 
     companions = {}
     for name in [c for c in args.companions.split(",") if c and c != args.config]:
-        cw = Workload(name, args, log)
-        cm = measure(cw, args.rho, args.steps, args.warmup, graph=bool(args.graph))
-        companions[name] = summary(cw, cm, args.rho)
-        log(f"{name}: {cm['step_us']:.1f} us/step, {cm['value']:.0f} GB/s, ffn {cm['fwd_us']:.1f} us "
-            f"({cm['fwd_gbs']:.0f} GB/s), routed {cm['routed']:.1f}")
-        cw.free()
+        companions[name] = companion_run(name, args, log)
 
     head = summary(wl, main_m, args.rho)
     line = {

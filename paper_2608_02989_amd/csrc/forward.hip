@@ -1139,12 +1139,14 @@ __global__ __launch_bounds__(256) void combine_kernel(ForwardParams p, int hbloc
   reinterpret_cast<float4*>(p.out + static_cast<size_t>(t) * H)[h4] = s;
 }
 
-// Workgroups of `kernel` (256 threads) resident on the current device at
-// once, computed on first use per device.
-template <class F>
-int resident_workgroups(F kernel) {
+// Workgroups of kernel `Kern` (256 threads) resident on the current device at
+// once, computed on first use per kernel and device (a template per kernel, so
+// kernels of different register or LDS needs keep separate counts).
+template <auto Kern>
+int resident_workgroups() {
   constexpr int kMaxDevices = 64;
   static int cached[kMaxDevices] = {};
+  const auto kernel = Kern;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = 0;
   if (cached[dev] == 0) {
@@ -1163,12 +1165,12 @@ hipError_t launch_gate_up(const ForwardParams& p, int cap, bool self, hipStream_
   if (!self) {
     ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, false, 8><<<dim3(items), 256, 0, stream>>>(p);
   } else if (p.k <= 8) {
-    auto kern = ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, 8>;
-    const int res = (p.H >= 4096 ? kSelfGridMult : 1) * resident_workgroups(kern);
+    constexpr auto kern = &ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, 8>;
+    const int res = (p.H >= 4096 ? kSelfGridMult : 1) * resident_workgroups<kern>();
     kern<<<dim3(items < res ? items : res), 256, 0, stream>>>(p);
   } else {
-    auto kern = ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, kMaxTopK>;
-    const int res = (p.H >= 4096 ? kSelfGridMult : 1) * resident_workgroups(kern);
+    constexpr auto kern = &ffn_kernel<P, Proj::GateUp, MTMAX, AMOE_GU_NTW, AMOE_GU_KS, true, kMaxTopK>;
+    const int res = (p.H >= 4096 ? kSelfGridMult : 1) * resident_workgroups<kern>();
     kern<<<dim3(items < res ? items : res), 256, 0, stream>>>(p);
   }
   return hipGetLastError();
