@@ -410,6 +410,30 @@ def test_forward_parity_path_limits(gpu, T, k, E, dtype):
     check_forward(got, ref, cfg.dtype, f"limits T={T} k={k} E={E}")
 
 
+# blocks of more than 256 tokens: experts with more than 4 M-tiles of tokens run
+# their waves as 2 or 4 M groups over one weight stream.  Token counts 70, 100,
+# 130, 260 and 40 give the gate/up pass M groups of 2 x 3, 2 x 4 and 4 x 3
+# M-tiles and a 4 x 4 pass followed by a single M-tile, and the down pass 2 x 3,
+# 2 x 4 and repeated 2 x 4 passes with ragged remainders.
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_forward_parity_m_groups(gpu, dtype):
+    T, k, E = 300, 2, 8
+    cfg = W.LayerConfig("mgroups", 171 + (dtype == "f32"), dtype, T=T, B=1, H=256, E=E, k=k, I=128,
+                        depth_max=6, commit_rule="depth_sibling", hidden_std=1.0)
+    t = np.arange(T)
+    slot0 = np.where(t < 70, 0, np.where(t < 170, 1, 2))
+    slot1 = np.where(t < 260, 3, 4)
+    idx = np.stack([slot0, slot1], axis=1).astype(np.int32)
+    assert np.bincount(idx.reshape(-1), minlength=E).tolist() == [70, 100, 130, 260, 40, 0, 0, 0]
+    rng = np.random.default_rng(77)
+    gate = rng.random((T, k)).astype(np.float32)
+    h32 = rng.standard_normal((T, cfg.H)).astype(np.float32)
+    say(f"forward M groups T={T} dtype={dtype}")
+    got, h64, (wg, wu, wd) = forward_case(cfg, idx, gate, h32)
+    ref = O.moe_forward_grouped(h64, wg, wu, wd, idx, gate, cfg.dtype)
+    check_forward(got, ref, cfg.dtype, f"M groups {dtype}")
+
+
 # one GPU's share of a tensor-parallel split over I: thin I gives the column-tile
 # down pass 3-step stages (one column tile at H = 1024, two at H = 4096)
 @pytest.mark.parametrize("H,I,T,E", [(1024, 96, 32, 64), (4096, 192, 64, 32)])
